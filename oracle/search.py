@@ -1,0 +1,163 @@
+"""Alg. 1 (Var-Stream) and its settings Fixed / Var-Batch, fp64 (test
+infrastructure; see oracle/__init__).
+
+Decode(X, E, D, n, eps, k, H) (Sec. 3, Alg. 1):
+  c = first unadmitted input; beams B; outputs Y
+  while inputs remain or B is non-empty:
+      if inputs remain and |B| <= eps * n:
+          encode and admit m new inputs (fresh beams holding the start symbol)
+      select the beams with minimal l_t (steps taken)
+      expand every candidate of the selected beams with D; update each
+      selected beam (top-k, H, finalization); a beam whose candidates are
+      all terminated is finished and its candidates become Y[i]
+      remove finished beams
+
+Readings (listed with the design notes): the refill admits
+m = min(n - |B|, inputs left), i.e. it refills the batch to n (Sec. 3: the
+initial batch is n and a refill restores size n); inputs are admitted in
+index order; Var-Batch is eps = 0 (refill only when the batch is empty) and
+Fixed is eps = 0, delta = inf, M = k (App. A.1: Fixed-Ours is eps = 0).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+
+from .beam import ACTIVE, Cand, beam_step
+
+
+@dataclasses.dataclass
+class Hyp:
+    tokens: tuple
+    score: float
+    status: int
+
+
+@dataclasses.dataclass
+class SearchResult:
+    hyps: List[List[Hyp]]               # Y[i], rank order
+    finalize_step: np.ndarray           # global timestep at which input i finished
+    steps_taken: np.ndarray             # l_t of input i's beam when it finished
+    min_margin: np.ndarray              # smallest decision margin over input i's steps
+    margins: List[List[float]]          # per input, per own step: min margin of that step
+    widths: List[List[int]]             # per input, per own step: rows expanded
+    timesteps: int = 0
+    expansions: int = 0
+    noops: int = 0
+    refills: int = 0
+    admitted: int = 0
+    rows_per_step: List[int] = dataclasses.field(default_factory=list)
+
+    @property
+    def n_hyps(self) -> int:
+        return sum(len(y) for y in self.hyps)
+
+    def stats(self) -> dict:
+        return dict(timesteps=self.timesteps, expansions=self.expansions,
+                    noops=self.noops, refills=self.refills,
+                    admitted=self.admitted, hyps=self.n_hyps)
+
+
+@dataclasses.dataclass
+class _Beam:
+    input: int
+    steps: int
+    cands: List[Cand]
+
+
+def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
+           n: int, eps: float, k: int, delta: float = math.inf,
+           M: Optional[int] = None, on_step: Optional[Callable] = None) -> SearchResult:
+    """Run Alg. 1 over inputs 0..N-1 (h0[i] is e_i = E(x_i)).
+
+    `decoder` needs initial_state(h0_row) and expand(h_prev, y, t, Lx) ->
+    (h, lp) as in oracle.decoder.ElmanDecoder (tests substitute scripted
+    decoders). `on_step(timestep, selected_inputs, rows)` observes the
+    schedule.
+    """
+    N = len(Lx)
+    M = k if M is None else int(M)
+    if not (k >= 1 and n >= 1 and 0.0 <= eps < 1.0 and 1 <= M <= k):
+        raise ValueError("invalid search parameters")
+    res = SearchResult(hyps=[None] * N, finalize_step=np.zeros(N, np.int64),
+                       steps_taken=np.zeros(N, np.int64),
+                       min_margin=np.full(N, np.inf),
+                       margins=[[] for _ in range(N)], widths=[[] for _ in range(N)])
+    c = 0
+    live: List[_Beam] = []
+    while c < N or live:
+        if c < N and len(live) <= eps * n:
+            m = min(n - len(live), N - c)
+            for i in range(c, c + m):
+                st = decoder.initial_state(h0[i])
+                live.append(_Beam(i, 0, [Cand(0.0, (), ACTIVE, st, 0)]))
+            c += m
+            res.refills += 1
+            res.admitted += m
+        lmin = min(b.steps for b in live)
+        sel = [b for b in live if b.steps == lmin]
+
+        # One batched decoder call over every active candidate of the
+        # selected beams (the inner loops of Alg. 1).
+        rows = [(bi, j) for bi, b in enumerate(sel)
+                for j, cand in enumerate(b.cands) if cand.status == ACTIVE]
+        h_prev = np.stack([sel[bi].cands[j].h for bi, j in rows])
+        y = np.array([sel[bi].cands[j].y for bi, j in rows])
+        t = np.array([sel[bi].steps + 1 for bi, _ in rows])
+        lx = np.array([Lx[sel[bi].input] for bi, _ in rows])
+        h_new, lp = decoder.expand(h_prev, y, t, lx)
+        res.timesteps += 1
+        res.expansions += len(rows)
+        res.rows_per_step.append(len(rows))
+        if on_step is not None:
+            on_step(res.timesteps, [b.input for b in sel], len(rows))
+
+        per_beam_lp: Dict[int, dict] = {}
+        per_beam_h: Dict[int, dict] = {}
+        for r, (bi, j) in enumerate(rows):
+            per_beam_lp.setdefault(bi, {})[j] = lp[r]
+            per_beam_h.setdefault(bi, {})[j] = h_new[r]
+        finished = []
+        for bi, b in enumerate(sel):
+            res.noops += sum(1 for cand in b.cands if cand.status != ACTIVE)
+            out = beam_step(b.cands, per_beam_lp.get(bi, {}), per_beam_h.get(bi, {}),
+                            b.steps + 1, int(max_len[b.input]), k, delta, M)
+            res.widths[b.input].append(sum(1 for cand in b.cands if cand.status == ACTIVE))
+            res.margins[b.input].append(out.margin)
+            res.min_margin[b.input] = min(res.min_margin[b.input], out.margin)
+            b.cands = out.beam
+            b.steps += 1
+            if out.ended:
+                res.hyps[b.input] = [Hyp(cd.tokens, cd.score, cd.status) for cd in out.beam]
+                res.finalize_step[b.input] = res.timesteps
+                res.steps_taken[b.input] = b.steps
+                finished.append(b)
+        if finished:
+            done = set(id(b) for b in finished)
+            live = [b for b in live if id(b) not in done]
+    return res
+
+
+def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var_stream",
+                    inputs: Optional[Sequence[int]] = None, decoder=None) -> SearchResult:
+    """Convenience wrapper: decode (a subset of) a synthgen Workload with its
+    config's parameters; `sched` picks Fixed / Var-Batch / Var-Stream."""
+    from .decoder import ElmanDecoder
+    c = wl.cfg
+    dec = decoder or ElmanDecoder.from_workload(wl)
+    n = c.n if n is None else n
+    k = c.k if k is None else k
+    eps = c.eps if eps is None else eps
+    delta = c.delta if delta is None else delta
+    M = c.M if M is None else M
+    if sched == "fixed":
+        eps, delta, M = 0.0, math.inf, k
+    elif sched == "var_batch":
+        eps = 0.0
+    elif sched != "var_stream":
+        raise ValueError(sched)
+    idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
+    return decode(dec, wl.h0[idx], wl.Lx[idx], wl.max_len[idx], n, eps, k, delta, M)

@@ -1,0 +1,95 @@
+"""Planted mistakes in the oracle must be caught by its pins.
+
+Each case rewrites one expression of an oracle module (a flipped sign, a
+transposed operand, a dropped term, a changed comparison or selection rule),
+loads the mutant, and checks that the named pin tests now fail. This shows
+the pins constrain the oracle beyond restating it. CPU only."""
+import importlib
+import inspect
+import json
+import os
+import types
+
+import pytest
+
+import oracle.decoder
+import oracle.search
+import tests.test_oracle_decoder as tdec
+import tests.test_oracle_search as tsearch
+
+
+def _mutant(modname, old, new):
+    mod = importlib.import_module(f"oracle.{modname}")
+    src = inspect.getsource(mod)
+    assert src.count(old) == 1, f"mutation anchor not unique in oracle.{modname}: {old}"
+    m = types.ModuleType(f"oracle.{modname}")
+    m.__dict__["__package__"] = "oracle"
+    exec(compile(src.replace(old, new), f"<mutant oracle.{modname}>", "exec"), m.__dict__)
+    return m
+
+
+def _cases():
+    with open(os.path.join(os.path.dirname(__file__), "golden", "scripted_beam_cases.json")) as f:
+        return {c["name"]: c for c in json.load(f)["cases"]}
+
+
+PINS = {
+    "zero_weights": lambda: tdec.test_zero_weights_leave_only_eos_bias(9, 5, 1.0),
+    "log_softmax": tdec.test_log_softmax_closed_forms,
+    "orientation": tdec.test_recurrence_orientation_and_embedding_row,
+    "proj_orientation": tdec.test_output_projection_orientation,
+    "exhaustive": lambda: tsearch.test_exhaustive_beam_returns_every_complete_output_sorted(3, 4, 1, False),
+    "greedy": lambda: tsearch.test_k1_is_greedy(0),
+    "falls_off": lambda: tsearch.test_scripted_cases(_cases()["finalized_candidate_falls_off"]),
+    "threshold_ref": lambda: tsearch.test_scripted_cases(_cases()["threshold_reference_is_terminated"]),
+    "max_per_node": lambda: tsearch.test_scripted_cases(_cases()["max_candidates_per_node_and_maxlen"]),
+    "noop": lambda: tsearch.test_scripted_cases(_cases()["noop_keeps_terminated_rank"]),
+    "ties": lambda: tsearch.test_scripted_cases(_cases()["exact_ties_follow_rank_key"]),
+    "fig1": tsearch.test_fig1_schedule,
+    "stream_vs_batch": lambda: tsearch.test_var_stream_matches_var_batch(0, 4, 0.25),
+}
+
+MUTATIONS = [
+    ("eos_bias_sign", "decoder",
+     "self.beta * (np.asarray(t, np.float64) - np.asarray(Lx, np.float64))",
+     "self.beta * (np.asarray(Lx, np.float64) - np.asarray(t, np.float64))", ["zero_weights"]),
+    ("bias_on_wrong_token", "decoder", "z[:, self.eos] +=", "z[:, 1] +=", ["zero_weights"]),
+    ("transposed_recurrence", "decoder", "h_prev @ self.W_h.T", "h_prev @ self.W_h", ["orientation"]),
+    ("dropped_embedding", "decoder", "h_prev @ self.W_h.T + self.E[np.asarray(y)]",
+     "h_prev @ self.W_h.T", ["orientation"]),
+    ("dropped_normalizer", "decoder", "return z - (m + np.log(s))", "return z - m",
+     ["log_softmax", "zero_weights"]),
+    ("reference_is_best_active", "beam", "ref = full[0][0]",
+     "ref = next((e[0] for e in full if e[2] != NOOP_TOKEN), full[0][0])", ["threshold_ref"]),
+    ("terminated_not_carried", "beam", "pool.append((c.score, j, NOOP_TOKEN))", "pass",
+     ["noop", "exhaustive"]),
+    ("max_per_node_ignored", "beam", "if per_parent.get(j, 0) >= M:", "if False:", ["max_per_node"]),
+    ("maxlen_off_by_one", "beam", "elif t == max_len:", "elif t == max_len - 1:",
+     ["max_per_node", "exhaustive"]),
+    ("parent_rank_tiebreak_reversed", "beam", "pool.sort(key=lambda e: (-e[0], e[1], e[2]))",
+     "pool.sort(key=lambda e: (-e[0], -e[1], e[2]))", ["ties"]),
+    ("token_tiebreak_reversed", "beam", "pool.sort(key=lambda e: (-e[0], e[1], e[2]))",
+     "pool.sort(key=lambda e: (-e[0], e[1], -e[2]))", ["ties"]),
+    ("refill_strict", "search", "len(live) <= eps * n", "len(live) < eps * n", ["fig1"]),
+    ("expand_all_live", "search", "sel = [b for b in live if b.steps == lmin]", "sel = list(live)", ["fig1"]),
+    ("bias_uses_global_timestep", "search", "t = np.array([sel[bi].steps + 1 for bi, _ in rows])",
+     "t = np.array([res.timesteps + 1 for bi, _ in rows])", ["stream_vs_batch", "greedy"]),
+]
+
+
+@pytest.mark.parametrize("name,modname,old,new,pins", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_planted_mistake_is_caught(monkeypatch, name, modname, old, new, pins):
+    mut = _mutant(modname, old, new)
+    if modname == "decoder":
+        for target in (oracle.decoder, tdec, tsearch):
+            for attr in ("ElmanDecoder", "log_softmax"):
+                if hasattr(target, attr):
+                    monkeypatch.setattr(target, attr, getattr(mut, attr))
+    elif modname == "beam":
+        monkeypatch.setattr(oracle.search, "beam_step", mut.beam_step)
+    else:
+        for attr in ("decode", "decode_workload"):
+            monkeypatch.setattr(tsearch, attr, getattr(mut, attr))
+    for pin in pins:
+        with pytest.raises(Exception):
+            PINS[pin]()
