@@ -1,0 +1,197 @@
+/*
+ * streambeam -- streaming variable-width batched beam search on MI355X (gfx950).
+ *
+ * C ABI of the decoding library. It implements the per-timestep batched
+ * beam-search step of Var-Stream (Yang et al., "A Streaming Approach For
+ * Efficient Batched Beam Search", EMNLP 2020, Sec. 3 and Alg. 1) and its
+ * settings Fixed and Var-Batch, on a synthetic Elman decoder
+ *     h = tanh(W_h h_prev + E[y]),  z = W_out h,  z[0] += beta (t - L_x),
+ *     log-probabilities = z - logsumexp(z)      (the decoder D of Sec. 2).
+ * The calls follow Alg. 1's problem statement Decode(X, E, D, n, eps, k, H):
+ * create a decoder with (k, n, eps, H), submit inputs, step, collect the
+ * finalized hypotheses Y.
+ *
+ * Conventions for every entry point:
+ *  - Device pointers are HIP device addresses on the current device; host
+ *    pointers are ordinary process memory. The header needs no HIP headers:
+ *    streams are passed as void* (a hipStream_t, or NULL for the default
+ *    stream).
+ *  - The caller owns all device memory (weights, the workspace, h0 staging);
+ *    it must outlive the decoder. The library never allocates or frees device
+ *    memory; it owns a small host-side object, pinned host staging for the
+ *    per-input lengths (8 bytes per queue entry) and a few HIP events.
+ *  - All device work is ordered on the decoder's stream.
+ *  - No call aborts or throws across the ABI. Errors return an sb_status;
+ *    sb_last_error() gives the text of the decoder's last failure.
+ *  - A decoder is not thread-safe; distinct decoders are independent.
+ */
+#ifndef STREAMBEAM_H
+#define STREAMBEAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SB_OK = 0,
+  SB_E_INVALID_ARG = 1,   /* a pointer, size or parameter is out of range       */
+  SB_E_WORKSPACE = 2,     /* workspace missing, misaligned or too small          */
+  SB_E_STATE = 3,         /* call not valid in the decoder's current state       */
+  SB_E_QUEUE_FULL = 4,    /* submit would exceed params.max_inputs                */
+  SB_E_TRUNCATED = 5,     /* collect buffers full; the rest stays pending        */
+  SB_E_HIP = 6,           /* a HIP runtime call failed (text in sb_last_error)   */
+  SB_E_UNSUPPORTED = 7    /* shape or option this build does not implement       */
+} sb_status;
+
+/* Schedulers of Sec. 3 / Alg. 1. Fixed = fixed-width search with the
+ * paper's own finalization rule (App. A.1: eps = 0, no pruning); Var-Batch =
+ * variable-width search, refill only when the batch is empty (eps = 0);
+ * Var-Stream = refill when at most eps*n beams remain, expand only the beams
+ * with the fewest steps taken. */
+typedef enum { SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2 } sb_sched;
+
+/* Storage type of weights, h0 and decoder states. SB_F32: fp32 everywhere
+ * (MFMA fp32, fp32 accumulation). SB_BF16: bf16 weights and states; the
+ * projection accumulates in fp32, the recurrence pre-activation in fp64
+ * (exact for bf16 products) so that the rounded bf16 state is reproducible. */
+typedef enum { SB_F32 = 0, SB_BF16 = 1 } sb_dtype;
+
+/* Status of a finalized hypothesis. */
+enum { SB_HYP_EOS = 2, SB_HYP_MAXLEN = 3 };
+
+/* Search parameters (Alg. 1 inputs n, eps, k, H; Sec. 4 heuristics). */
+typedef struct {
+  int32_t k;             /* beam width, 1..16                                      */
+  int32_t n;             /* batch size: beams resident at once, >= 1               */
+  double  eps;           /* refill threshold in [0,1): refill when live <= eps*n   */
+  double  delta;         /* relative threshold (nats): drop y if score(y) <
+                            score(best) - delta; +inf disables (Sec. 4, App. A.3) */
+  int32_t max_per_node;  /* M: max kept expansions per parent per step, 1..k      */
+  int32_t sched;         /* sb_sched; SB_FIXED forces eps=0, delta=+inf, M=k;
+                            SB_VAR_BATCH forces eps=0                             */
+  int32_t max_len_cap;   /* upper bound on every input's max_len, 1..4096         */
+  int32_t max_inputs;    /* queue capacity (inputs per decoder lifetime/reset)    */
+} sb_params;
+
+/* Synthetic decoder D (Sec. 2). Token 0 is EOS and also the start symbol.
+ * Device arrays, row-major, element type per `dtype` (float or bf16 bits):
+ *   W_h   [d][d]     h = tanh(W_h h_prev + E[y])
+ *   E     [vocab][d] token embeddings
+ *   W_out [vocab][d] z[v] = sum_j W_out[v][j] h[j]
+ *   W_kv  [kv_layers][2][d][d] (bf16 only, or NULL): each expansion appends
+ *         the rows bf16(h . W_kv[l][j]) to the candidate's KV-like state. */
+typedef struct {
+  int32_t vocab;         /* |V| >= 2                                               */
+  int32_t d;             /* state size, multiple of 32, 32..4096                  */
+  int32_t dtype;         /* sb_dtype                                               */
+  float   eos_beta;      /* EOS bias slope beta                                    */
+  const void *W_h, *E, *W_out;
+  int32_t kv_layers;     /* 0, or 1..8 with dtype SB_BF16                          */
+  const void *W_kv;
+} sb_model;
+
+/* One finalized hypothesis y_ij of Y[i] (Alg. 1 output). */
+typedef struct {
+  int64_t input;         /* queue position of its input (submission order)         */
+  int32_t rank;          /* position in Y[i] (0 = best)                            */
+  int32_t length;        /* number of tokens, EOS included when present            */
+  int32_t status;        /* SB_HYP_EOS or SB_HYP_MAXLEN                             */
+  int32_t finalize_step; /* global timestep at which its beam finished            */
+  double  score;         /* cumulative natural-log probability                     */
+  int64_t tok_offset;    /* offset of its tokens in the collect token buffer       */
+} sb_hyp;
+
+/* Counters of Table 5's columns: timesteps, candidate expansions (decoder
+ * evaluations of one active candidate), plus no-op expansions of terminated
+ * candidates, refills, admitted inputs, finalized hypotheses, finished inputs. */
+typedef struct {
+  int64_t timesteps, expansions, noops, refills, admitted, hyps, finished;
+} sb_stats_t;
+
+typedef struct sb_decoder sb_decoder;
+
+/* Bytes of device workspace a decoder with this model/params needs (0 if the
+ * arguments are invalid). Host-only arithmetic: needs no GPU. */
+size_t sb_workspace_bytes(const sb_model *model, const sb_params *params);
+
+/* Check model/params without touching the GPU. Returns SB_OK or the error
+ * sb_create would return for them. */
+sb_status sb_validate(const sb_model *model, const sb_params *params);
+
+/* Create a decoder over a caller-owned device workspace of `bytes` bytes
+ * (>= sb_workspace_bytes, 256-byte aligned). The workspace is initialised on
+ * `stream`; the weights are read, never written. The KV path keeps a
+ * transposed copy of W_kv in the workspace. */
+sb_status sb_create(const sb_model *model, const sb_params *params, void *workspace,
+                    size_t bytes, void *stream, sb_decoder **out);
+
+/* Append `count` inputs to the queue (Alg. 1's X, in index order).
+ * h0: device [count][d] (dtype of the model), the encodings e_i = E(x_i),
+ * copied asynchronously on the stream (the caller may reuse it once the
+ * stream has passed this point). L_x, max_len: host [count], copied before
+ * return; 1 <= max_len[i] <= max_len_cap. */
+sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_t *L_x,
+                    const int32_t *max_len);
+
+/* Enqueue one timestep of Alg. 1's loop (refill, select, expand, update,
+ * finalize). If `done` is non-NULL, synchronizes and stores 1 when no input
+ * is pending and no beam is live, else 0. With done == NULL nothing waits. */
+sb_status sb_step(sb_decoder *dec, int32_t *done);
+
+/* Step until every submitted input is finished; returns after the stream has
+ * completed the work. */
+sb_status sb_run(sb_decoder *dec);
+
+/* Copy finalized hypotheses to the host, in input order then rank order,
+ * starting at the first not-yet-collected input and stopping at the first
+ * unfinished one. Token ids of hypothesis h are tokens[h.tok_offset ..
+ * h.tok_offset + h.length). Returns SB_E_TRUNCATED (with everything that fit)
+ * when a buffer is too small; the rest stays pending for the next call.
+ * Synchronizes the stream. */
+sb_status sb_collect(sb_decoder *dec, sb_hyp *hyps, int64_t hyp_cap, int32_t *tokens,
+                     int64_t tok_cap, int64_t *n_hyps, int64_t *n_tokens);
+
+/* Counters since create/reset. Synchronizes the stream. */
+sb_status sb_stats(sb_decoder *dec, sb_stats_t *out);
+
+/* Forget all inputs, beams, outputs and counters (the queue restarts at
+ * position 0). Asynchronous on the stream. */
+sb_status sb_reset(sb_decoder *dec);
+
+/* Enable (1) or disable (0) per-kernel timing with HIP events on the
+ * decoder's stream around the vocabulary-projection kernel of every step. */
+sb_status sb_set_timing(sb_decoder *dec, int32_t enable);
+
+/* Sum of the timed projection-kernel durations (ms) and the number of timed
+ * launches since timing was enabled. Synchronizes the stream. */
+sb_status sb_timing(sb_decoder *dec, double *proj_ms, int64_t *proj_launches);
+
+/* Debug view of one candidate slot after the last step (test support):
+ * status, score, its tokens so far (up to tok_cap) and, with a KV state, its
+ * KV rows [layers][2][steps][d] as bf16 bits (up to kv_cap elements). */
+/* Test support: run one decoder step (recurrence, projection, row merge)
+ * on R explicit rows, outside any search. Valid only on a decoder with no
+ * live beams (after create/reset/run); it leaves the decoder reset.
+ * h_prev: device [R][d] (model dtype); y, t, L_x: host [R] (last token,
+ * 1-based emitted position, input length); R <= n*k. Outputs: h_out device
+ * [R][d] (model dtype), lse host [R], top_lp host [R][k] (log-probabilities
+ * of the row's best k tokens, best first), top_tok host [R][k]. */
+sb_status sb_debug_expand(sb_decoder *dec, int32_t R, const void *h_prev, const int32_t *y,
+                          const int32_t *t, const int32_t *L_x, void *h_out, double *lse,
+                          double *top_lp, int32_t *top_tok);
+
+sb_status sb_debug_slot(sb_decoder *dec, int32_t beam, int32_t rank, int32_t *status,
+                        double *score, int64_t *input, int32_t *steps, int32_t *tokens,
+                        int32_t tok_cap, int32_t *n_tokens, uint16_t *kv, int64_t kv_cap);
+
+sb_status sb_destroy(sb_decoder *dec);
+const char *sb_last_error(const sb_decoder *dec);
+const char *sb_status_string(sb_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STREAMBEAM_H */

@@ -1,0 +1,604 @@
+// Host side of the streambeam C ABI: validation, workspace carve-up, the
+// per-timestep launch sequence of Alg. 1 and result collection.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/streambeam.h"
+#include "sb_internal.h"
+
+using namespace sb;
+
+struct sb_decoder {
+  sb_model model;
+  sb_params params;
+  DevState st;
+  hipStream_t stream;
+  unsigned char *ws;
+  size_t ws_bytes;
+  int32_t n_queued = 0;
+  int32_t collected = 0;       // inputs already returned by sb_collect
+  int32_t *pinned_len = nullptr;   // [2][max_inputs] L_x and max_len staging
+  int32_t *pinned_flag = nullptr;  // [2] done-flag readback
+  hipEvent_t poll_ev[2] = {nullptr, nullptr};
+  bool timing = false;
+  std::vector<hipEvent_t> tev;  // pairs around the projection kernel
+  int tev_used = 0;
+  double proj_ms = 0.0;
+  int64_t proj_launches = 0;
+  std::string err;
+};
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+
+struct Layout {
+  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, s_status, s_score, s_tok, s_h,
+      s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
+      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, total;
+};
+
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+int kbucket_of(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
+
+Layout layout_of(const sb_model &m, const sb_params &p) {
+  Layout L{};
+  const size_t es = m.dtype == SB_BF16 ? 2 : 4;
+  const size_t n = p.n, k = p.k, d = m.d, nk = n * k, Rm = nk;
+  const size_t S = proj_tiles(m.vocab);
+  const size_t KB = kbucket_of(p.k);
+  const size_t Q = p.max_inputs, MLC = p.max_len_cap;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += up(bytes);
+    return o;
+  };
+  L.ctrl = take(sizeof(DevCtrl));
+  L.q_h0 = take(Q * d * es);
+  L.q_Lx = take(Q * 4);
+  L.q_ml = take(Q * 4);
+  L.b_input = take(n * 4);
+  L.b_steps = take(n * 4);
+  L.b_sel = take(n * 4);
+  L.b_par = take(n * 4);
+  L.s_status = take(nk * 4);
+  L.s_score = take(nk * 8);
+  L.s_tok = take(nk * 4);
+  L.s_h = take(nk * d * es);
+  L.s_row = take(nk * 4);
+  L.s_prow = take(nk * 4);
+  L.bp = take(Q * MLC * k * 4);
+  L.r_slot = take(Rm * 4);
+  L.r_hsrc = take(Rm * 4);
+  L.r_y = take(Rm * 4);
+  L.r_t = take(Rm * 4);
+  L.r_Lx = take(Rm * 4);
+  L.r_lse = take(Rm * 8);
+  L.hbuf = take(Rm * d * es);
+  L.part = take(Rm * S * (2 + 2 * KB) * 4);
+  L.top_lp = take(Rm * k * 8);
+  L.top_tok = take(Rm * k * 4);
+  L.o_count = take(Q * 4);
+  L.o_hyp = take(Q * k * sizeof(OutHyp));
+  L.o_tok = take(Q * k * MLC * 4);
+  if (m.kv_layers > 0) {
+    const size_t planes = (size_t)m.kv_layers * 2;
+    L.kv0 = take(nk * planes * MLC * d * 2);
+    L.kv1 = take(nk * planes * MLC * d * 2);
+    L.kvnew = take(Rm * planes * d * 2);
+    L.wkvT = take(planes * d * d * 2);
+  }
+  L.total = off;
+  return L;
+}
+
+sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
+  auto bad = [&](sb_status s, const char *msg) {
+    if (why) *why = msg;
+    return s;
+  };
+  if (!m || !p) return bad(SB_E_INVALID_ARG, "null model or params");
+  if (m->dtype != SB_F32 && m->dtype != SB_BF16) return bad(SB_E_INVALID_ARG, "unknown dtype");
+  if (m->d < 32 || m->d > 4096 || m->d % 32) return bad(SB_E_UNSUPPORTED, "d must be a multiple of 32 in [32, 4096]");
+  if (m->dtype == SB_BF16 && m->d % 64) return bad(SB_E_UNSUPPORTED, "bf16 needs d a multiple of 64");
+  if (p->k < 1 || p->k > KMAX_SUPPORTED) return bad(SB_E_UNSUPPORTED, "k must be in [1, 16]");
+  if (m->vocab < 2 || m->vocab < p->k || m->vocab > (1 << 23)) return bad(SB_E_INVALID_ARG, "vocab must be in [max(2,k), 2^23]");
+  if (!(p->n >= 1 && p->n <= 4096)) return bad(SB_E_UNSUPPORTED, "n must be in [1, 4096]");
+  if ((int64_t)p->n * p->k > 65536) return bad(SB_E_UNSUPPORTED, "n*k must be <= 65536");
+  if (!(p->eps >= 0.0 && p->eps < 1.0)) return bad(SB_E_INVALID_ARG, "eps must be in [0, 1)");
+  if (!(p->delta > 0.0)) return bad(SB_E_INVALID_ARG, "delta must be > 0 (use +inf to disable)");
+  if (p->max_per_node < 1 || p->max_per_node > p->k) return bad(SB_E_INVALID_ARG, "max_per_node must be in [1, k]");
+  if (p->sched < SB_FIXED || p->sched > SB_VAR_STREAM) return bad(SB_E_INVALID_ARG, "unknown scheduler");
+  if (p->max_len_cap < 1 || p->max_len_cap > 4096) return bad(SB_E_INVALID_ARG, "max_len_cap must be in [1, 4096]");
+  if (p->max_inputs < 1) return bad(SB_E_INVALID_ARG, "max_inputs must be >= 1");
+  if (m->kv_layers < 0 || m->kv_layers > 8) return bad(SB_E_UNSUPPORTED, "kv_layers must be in [0, 8]");
+  if (m->kv_layers > 0 && m->dtype != SB_BF16) return bad(SB_E_UNSUPPORTED, "KV state requires bf16");
+  if (m->kv_layers > 0 && !m->W_kv) return bad(SB_E_INVALID_ARG, "W_kv is NULL");
+  return SB_OK;
+}
+
+// Effective search parameters of a scheduler (Sec. 3; App. A.1).
+sb_params effective(const sb_params &p) {
+  sb_params e = p;
+  if (p.sched == SB_FIXED) {
+    e.eps = 0.0;
+    e.delta = INFINITY;
+    e.max_per_node = p.k;
+  } else if (p.sched == SB_VAR_BATCH) {
+    e.eps = 0.0;
+  }
+  return e;
+}
+
+#define HIPCHK(expr)                                                       \
+  do {                                                                     \
+    hipError_t _e = (expr);                                                \
+    if (_e != hipSuccess) {                                                \
+      dec->err = std::string(#expr) + ": " + hipGetErrorString(_e);        \
+      return SB_E_HIP;                                                     \
+    }                                                                      \
+  } while (0)
+
+__global__ void k_set_queued(DevCtrl *c, int32_t nq) {
+  c->n_queued = nq;
+  if (c->cursor < nq) c->done = 0;
+}
+
+__global__ void k_set_rows(DevCtrl *c, int32_t R) { c->R = R; }
+
+sb_status launch_step(sb_decoder *dec) {
+  const DevState &st = dec->st;
+  hipStream_t s = dec->stream;
+  HIPCHK(launch_sched(st, s));
+  HIPCHK(launch_rec(st, s));
+  if (st.kv_layers > 0) HIPCHK(launch_kv_append(st, s));
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (dec->timing) {
+    if (dec->tev_used + 2 > (int)dec->tev.size()) {
+      // harvest the pool
+      HIPCHK(hipStreamSynchronize(s));
+      for (int i = 0; i + 1 < dec->tev_used; i += 2) {
+        float ms = 0.f;
+        HIPCHK(hipEventElapsedTime(&ms, dec->tev[i], dec->tev[i + 1]));
+        dec->proj_ms += ms;
+        dec->proj_launches += 1;
+      }
+      dec->tev_used = 0;
+    }
+    e0 = dec->tev[dec->tev_used];
+    e1 = dec->tev[dec->tev_used + 1];
+    dec->tev_used += 2;
+    HIPCHK(hipEventRecord(e0, s));
+  }
+  HIPCHK(launch_proj(st, s));
+  if (dec->timing) HIPCHK(hipEventRecord(e1, s));
+  HIPCHK(launch_rowmerge(st, s));
+  HIPCHK(launch_beam(st, s));
+  if (st.kv_layers > 0) HIPCHK(launch_kv_gather(st, s));
+  return SB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sb_status_string(sb_status s) {
+  switch (s) {
+    case SB_OK: return "ok";
+    case SB_E_INVALID_ARG: return "invalid argument";
+    case SB_E_WORKSPACE: return "workspace too small or misaligned";
+    case SB_E_STATE: return "invalid state";
+    case SB_E_QUEUE_FULL: return "input queue full";
+    case SB_E_TRUNCATED: return "output truncated";
+    case SB_E_HIP: return "HIP runtime error";
+    case SB_E_UNSUPPORTED: return "unsupported shape or option";
+  }
+  return "unknown status";
+}
+
+sb_status sb_validate(const sb_model *model, const sb_params *params) {
+  return check(model, params, nullptr);
+}
+
+size_t sb_workspace_bytes(const sb_model *model, const sb_params *params) {
+  if (check(model, params, nullptr) != SB_OK) return 0;
+  return layout_of(*model, *params).total;
+}
+
+const char *sb_last_error(const sb_decoder *dec) { return dec ? dec->err.c_str() : "null decoder"; }
+
+sb_status sb_create(const sb_model *model, const sb_params *params, void *workspace, size_t bytes,
+                    void *stream, sb_decoder **out) {
+  if (!out) return SB_E_INVALID_ARG;
+  *out = nullptr;
+  sb_status s = check(model, params, nullptr);
+  if (s != SB_OK) return s;
+  if (!model->W_h || !model->E || !model->W_out) return SB_E_INVALID_ARG;
+  const Layout L = layout_of(*model, *params);
+  if (!workspace || ((uintptr_t)workspace % ALIGN) != 0 || bytes < L.total) return SB_E_WORKSPACE;
+  sb_decoder *dec = new (std::nothrow) sb_decoder();
+  if (!dec) return SB_E_INVALID_ARG;
+  dec->model = *model;
+  dec->params = effective(*params);
+  dec->stream = static_cast<hipStream_t>(stream);
+  dec->ws = static_cast<unsigned char *>(workspace);
+  dec->ws_bytes = bytes;
+  DevState &st = dec->st;
+  unsigned char *w = dec->ws;
+  st.ctrl = reinterpret_cast<DevCtrl *>(w + L.ctrl);
+  st.q_h0 = w + L.q_h0;
+  st.q_Lx = reinterpret_cast<int32_t *>(w + L.q_Lx);
+  st.q_ml = reinterpret_cast<int32_t *>(w + L.q_ml);
+  st.b_input = reinterpret_cast<int32_t *>(w + L.b_input);
+  st.b_steps = reinterpret_cast<int32_t *>(w + L.b_steps);
+  st.b_sel = reinterpret_cast<int32_t *>(w + L.b_sel);
+  st.b_par = reinterpret_cast<int32_t *>(w + L.b_par);
+  st.s_status = reinterpret_cast<int32_t *>(w + L.s_status);
+  st.s_score = reinterpret_cast<double *>(w + L.s_score);
+  st.s_tok = reinterpret_cast<int32_t *>(w + L.s_tok);
+  st.s_h = w + L.s_h;
+  st.s_row = reinterpret_cast<int32_t *>(w + L.s_row);
+  st.s_prow = reinterpret_cast<int32_t *>(w + L.s_prow);
+  st.bp = reinterpret_cast<uint32_t *>(w + L.bp);
+  st.r_slot = reinterpret_cast<int32_t *>(w + L.r_slot);
+  st.r_hsrc = reinterpret_cast<int32_t *>(w + L.r_hsrc);
+  st.r_y = reinterpret_cast<int32_t *>(w + L.r_y);
+  st.r_t = reinterpret_cast<int32_t *>(w + L.r_t);
+  st.r_Lx = reinterpret_cast<int32_t *>(w + L.r_Lx);
+  st.r_lse = reinterpret_cast<double *>(w + L.r_lse);
+  st.hbuf = w + L.hbuf;
+  st.part = reinterpret_cast<float *>(w + L.part);
+  st.top_lp = reinterpret_cast<double *>(w + L.top_lp);
+  st.top_tok = reinterpret_cast<int32_t *>(w + L.top_tok);
+  st.o_count = reinterpret_cast<int32_t *>(w + L.o_count);
+  st.o_hyp = reinterpret_cast<OutHyp *>(w + L.o_hyp);
+  st.o_tok = reinterpret_cast<int32_t *>(w + L.o_tok);
+  if (model->kv_layers > 0) {
+    st.kv0 = reinterpret_cast<uint16_t *>(w + L.kv0);
+    st.kv1 = reinterpret_cast<uint16_t *>(w + L.kv1);
+    st.kvnew = reinterpret_cast<uint16_t *>(w + L.kvnew);
+    st.wkvT = reinterpret_cast<uint16_t *>(w + L.wkvT);
+  }
+  st.W_h = model->W_h;
+  st.E = model->E;
+  st.W_out = model->W_out;
+  const sb_params &p = dec->params;
+  st.n = p.n;
+  st.k = p.k;
+  st.d = model->d;
+  st.V = model->vocab;
+  st.M = p.max_per_node;
+  st.max_len_cap = p.max_len_cap;
+  st.refill_thr = (int32_t)floor(p.eps * (double)p.n);   // live <= eps*n  <=>  live <= floor(eps*n)
+  st.S = proj_tiles(model->vocab);
+  st.R_max = p.n * p.k;
+  st.dtype = model->dtype;
+  st.kv_layers = model->kv_layers;
+  st.max_inputs = p.max_inputs;
+  st.kbucket = kbucket_of(p.k);
+  st.delta = p.delta;
+  st.beta = model->eos_beta;
+
+  auto fail = [&](sb_status code) {
+    sb_destroy(dec);
+    return code;
+  };
+  if (hipHostMalloc(reinterpret_cast<void **>(&dec->pinned_len), sizeof(int32_t) * 2 * (size_t)p.max_inputs,
+                    hipHostMallocDefault) != hipSuccess)
+    return fail(SB_E_HIP);
+  if (hipHostMalloc(reinterpret_cast<void **>(&dec->pinned_flag), sizeof(int32_t) * 2, hipHostMallocDefault) !=
+      hipSuccess)
+    return fail(SB_E_HIP);
+  for (int i = 0; i < 2; ++i)
+    if (hipEventCreateWithFlags(&dec->poll_ev[i], hipEventDisableTiming) != hipSuccess) return fail(SB_E_HIP);
+  if (launch_init(st, dec->stream) != hipSuccess) return fail(SB_E_HIP);
+  if (model->kv_layers > 0 &&
+      launch_transpose_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
+    return fail(SB_E_HIP);
+  *out = dec;
+  return SB_OK;
+}
+
+sb_status sb_reset(sb_decoder *dec) {
+  if (!dec) return SB_E_INVALID_ARG;
+  // Earlier submits may still be copying from the pinned length staging.
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  HIPCHK(launch_init(dec->st, dec->stream));
+  dec->n_queued = 0;
+  dec->collected = 0;
+  return SB_OK;
+}
+
+sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_t *L_x,
+                    const int32_t *max_len) {
+  if (!dec) return SB_E_INVALID_ARG;
+  if (count < 0 || (count > 0 && (!h0 || !L_x || !max_len))) {
+    dec->err = "sb_submit: bad count or null pointer";
+    return SB_E_INVALID_ARG;
+  }
+  if (count == 0) return SB_OK;
+  const sb_params &p = dec->params;
+  if ((int64_t)dec->n_queued + count > p.max_inputs) {
+    dec->err = "sb_submit: queue capacity exceeded";
+    return SB_E_QUEUE_FULL;
+  }
+  for (int i = 0; i < count; ++i) {
+    if (max_len[i] < 1 || max_len[i] > p.max_len_cap) {
+      dec->err = "sb_submit: max_len out of [1, max_len_cap]";
+      return SB_E_INVALID_ARG;
+    }
+  }
+  const int q0 = dec->n_queued;
+  const size_t es = dec->model.dtype == SB_BF16 ? 2 : 4;
+  const size_t rowbytes = (size_t)dec->model.d * es;
+  int32_t *lx = dec->pinned_len + q0;
+  int32_t *ml = dec->pinned_len + p.max_inputs + q0;
+  memcpy(lx, L_x, sizeof(int32_t) * count);
+  memcpy(ml, max_len, sizeof(int32_t) * count);
+  HIPCHK(hipMemcpyAsync(static_cast<unsigned char *>(dec->st.q_h0) + q0 * rowbytes, h0, count * rowbytes,
+                        hipMemcpyDeviceToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(dec->st.q_Lx + q0, lx, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(dec->st.q_ml + q0, ml, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
+  dec->n_queued += count;
+  hipLaunchKernelGGL(k_set_queued, dim3(1), dim3(1), 0, dec->stream, dec->st.ctrl, dec->n_queued);
+  HIPCHK(hipGetLastError());
+  return SB_OK;
+}
+
+sb_status sb_step(sb_decoder *dec, int32_t *done) {
+  if (!dec) return SB_E_INVALID_ARG;
+  sb_status s = launch_step(dec);
+  if (s != SB_OK) return s;
+  if (done) {
+    HIPCHK(hipMemcpyAsync(dec->pinned_flag, &dec->st.ctrl->done, sizeof(int32_t), hipMemcpyDeviceToHost,
+                          dec->stream));
+    HIPCHK(hipStreamSynchronize(dec->stream));
+    *done = dec->pinned_flag[0];
+  }
+  return SB_OK;
+}
+
+sb_status sb_run(sb_decoder *dec) {
+  if (!dec) return SB_E_INVALID_ARG;
+  // Every step either expands a live beam or is the final no-op, and a beam
+  // takes at most max_len_cap steps, so this bounds any correct run.
+  const int64_t limit = ((int64_t)dec->n_queued + dec->params.n) * (dec->params.max_len_cap + 1) + 64;
+  constexpr int BURST = 8;
+  int64_t steps = 0;
+  int slot = 0;
+  bool pending = false;
+  while (true) {
+    for (int i = 0; i < BURST; ++i) {
+      sb_status s = launch_step(dec);
+      if (s != SB_OK) return s;
+    }
+    steps += BURST;
+    HIPCHK(hipMemcpyAsync(dec->pinned_flag + slot, &dec->st.ctrl->done, sizeof(int32_t),
+                          hipMemcpyDeviceToHost, dec->stream));
+    HIPCHK(hipEventRecord(dec->poll_ev[slot], dec->stream));
+    // Poll the previous burst's flag while this burst runs.
+    if (pending) {
+      HIPCHK(hipEventSynchronize(dec->poll_ev[slot ^ 1]));
+      if (dec->pinned_flag[slot ^ 1]) break;
+    }
+    pending = true;
+    slot ^= 1;
+    if (steps > limit) {
+      dec->err = "sb_run: step limit exceeded without completion";
+      return SB_E_STATE;
+    }
+  }
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  return SB_OK;
+}
+
+sb_status sb_collect(sb_decoder *dec, sb_hyp *hyps, int64_t hyp_cap, int32_t *tokens, int64_t tok_cap,
+                     int64_t *n_hyps, int64_t *n_tokens) {
+  if (!dec || !n_hyps || !n_tokens || hyp_cap < 0 || tok_cap < 0 || (hyp_cap > 0 && !hyps) ||
+      (tok_cap > 0 && !tokens))
+    return SB_E_INVALID_ARG;
+  *n_hyps = 0;
+  *n_tokens = 0;
+  const int q0 = dec->collected, q1 = dec->n_queued;
+  if (q1 <= q0) return SB_OK;
+  const int k = dec->params.k, MLC = dec->params.max_len_cap;
+  HIPCHK(launch_backtrack(dec->st, q0, q1, dec->stream));
+  const int nq = q1 - q0;
+  std::vector<int32_t> cnt(nq);
+  std::vector<OutHyp> oh((size_t)nq * k);
+  HIPCHK(hipMemcpyAsync(cnt.data(), dec->st.o_count + q0, sizeof(int32_t) * nq, hipMemcpyDeviceToHost,
+                        dec->stream));
+  HIPCHK(hipMemcpyAsync(oh.data(), dec->st.o_hyp + (size_t)q0 * k, sizeof(OutHyp) * nq * k,
+                        hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  // Finished prefix and the part of it that fits the buffers.
+  int q_end = q0;
+  int64_t nh = 0, nt = 0;
+  bool truncated = false;
+  for (int q = q0; q < q1; ++q) {
+    const int c = cnt[q - q0];
+    if (c <= 0) break;
+    int64_t toks = 0;
+    for (int r = 0; r < c; ++r) toks += oh[(size_t)(q - q0) * k + r].length;
+    if (nh + c > hyp_cap || nt + toks > tok_cap) {
+      truncated = true;
+      break;
+    }
+    nh += c;
+    nt += toks;
+    q_end = q + 1;
+  }
+  if (q_end > q0) {
+    const size_t rows = (size_t)(q_end - q0) * k;
+    std::vector<int32_t> tk(rows * MLC);
+    HIPCHK(hipMemcpyAsync(tk.data(), dec->st.o_tok + (size_t)q0 * k * MLC, sizeof(int32_t) * rows * MLC,
+                          hipMemcpyDeviceToHost, dec->stream));
+    HIPCHK(hipStreamSynchronize(dec->stream));
+    int64_t h = 0, t = 0;
+    for (int q = q0; q < q_end; ++q) {
+      const int c = cnt[q - q0];
+      for (int r = 0; r < c; ++r) {
+        const OutHyp &o = oh[(size_t)(q - q0) * k + r];
+        sb_hyp &y = hyps[h++];
+        y.input = q;
+        y.rank = r;
+        y.length = o.length;
+        y.status = o.status;
+        y.finalize_step = o.finalize_step;
+        y.score = o.score;
+        y.tok_offset = t;
+        memcpy(tokens + t, tk.data() + ((size_t)(q - q0) * k + r) * MLC, sizeof(int32_t) * o.length);
+        t += o.length;
+      }
+    }
+  }
+  *n_hyps = nh;
+  *n_tokens = nt;
+  dec->collected = q_end;
+  return truncated ? SB_E_TRUNCATED : SB_OK;
+}
+
+sb_status sb_stats(sb_decoder *dec, sb_stats_t *out) {
+  if (!dec || !out) return SB_E_INVALID_ARG;
+  DevCtrl c;
+  HIPCHK(hipMemcpyAsync(&c, dec->st.ctrl, sizeof(DevCtrl), hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  out->timesteps = c.timesteps;
+  out->expansions = c.expansions;
+  out->noops = c.noops;
+  out->refills = c.refills;
+  out->admitted = c.admitted;
+  out->hyps = c.hyps;
+  out->finished = c.finished;
+  return SB_OK;
+}
+
+sb_status sb_set_timing(sb_decoder *dec, int32_t enable) {
+  if (!dec) return SB_E_INVALID_ARG;
+  if (enable && dec->tev.empty()) {
+    dec->tev.resize(2 * 2048, nullptr);
+    for (auto &e : dec->tev) HIPCHK(hipEventCreate(&e));
+  }
+  dec->timing = enable != 0;
+  dec->tev_used = 0;
+  dec->proj_ms = 0.0;
+  dec->proj_launches = 0;
+  return SB_OK;
+}
+
+sb_status sb_timing(sb_decoder *dec, double *proj_ms, int64_t *proj_launches) {
+  if (!dec || !proj_ms || !proj_launches) return SB_E_INVALID_ARG;
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  for (int i = 0; i + 1 < dec->tev_used; i += 2) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, dec->tev[i], dec->tev[i + 1]));
+    dec->proj_ms += ms;
+    dec->proj_launches += 1;
+  }
+  dec->tev_used = 0;
+  *proj_ms = dec->proj_ms;
+  *proj_launches = dec->proj_launches;
+  return SB_OK;
+}
+
+sb_status sb_debug_expand(sb_decoder *dec, int32_t R, const void *h_prev, const int32_t *y, const int32_t *t,
+                          const int32_t *L_x, void *h_out, double *lse, double *top_lp, int32_t *top_tok) {
+  if (!dec) return SB_E_INVALID_ARG;
+  const DevState &st = dec->st;
+  if (R < 1 || R > st.R_max || !h_prev || !y || !t || !L_x || !h_out || !lse || !top_lp || !top_tok)
+    return SB_E_INVALID_ARG;
+  const size_t es = st.dtype == 1 ? 2 : 4;
+  const size_t rowbytes = (size_t)st.d * es;
+  std::vector<int32_t> src(R);
+  for (int r = 0; r < R; ++r) src[r] = r;   // states placed in slots 0..R-1
+  HIPCHK(hipMemcpyAsync(st.s_h, h_prev, R * rowbytes, hipMemcpyDeviceToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(st.r_hsrc, src.data(), sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(st.r_y, y, sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(st.r_t, t, sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(st.r_Lx, L_x, sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));
+  hipLaunchKernelGGL(k_set_rows, dim3(1), dim3(1), 0, dec->stream, st.ctrl, R);
+  HIPCHK(hipGetLastError());
+  HIPCHK(launch_rec(st, dec->stream));
+  HIPCHK(launch_proj(st, dec->stream));
+  HIPCHK(launch_rowmerge(st, dec->stream));
+  HIPCHK(hipMemcpyAsync(h_out, st.hbuf, R * rowbytes, hipMemcpyDeviceToDevice, dec->stream));
+  HIPCHK(hipMemcpyAsync(lse, st.r_lse, sizeof(double) * R, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipMemcpyAsync(top_lp, st.top_lp, sizeof(double) * R * st.k, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipMemcpyAsync(top_tok, st.top_tok, sizeof(int32_t) * R * st.k, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  return sb_reset(dec);
+}
+
+sb_status sb_debug_slot(sb_decoder *dec, int32_t beam, int32_t rank, int32_t *status, double *score,
+                        int64_t *input, int32_t *steps, int32_t *tokens, int32_t tok_cap, int32_t *n_tokens,
+                        uint16_t *kv, int64_t kv_cap) {
+  if (!dec || !status || !score || !input || !steps || !n_tokens) return SB_E_INVALID_ARG;
+  const DevState &st = dec->st;
+  if (beam < 0 || beam >= st.n || rank < 0 || rank >= st.k) return SB_E_INVALID_ARG;
+  const int slot = beam * st.k + rank;
+  int32_t bin = -1, bst = 0, bpar = 0, sst = 0;
+  double ssc = 0.0;
+  HIPCHK(hipMemcpyAsync(&bin, st.b_input + beam, 4, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipMemcpyAsync(&bst, st.b_steps + beam, 4, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipMemcpyAsync(&bpar, st.b_par + beam, 4, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipMemcpyAsync(&sst, st.s_status + slot, 4, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipMemcpyAsync(&ssc, st.s_score + slot, 8, hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  *status = bin >= 0 ? sst : SLOT_EMPTY;
+  *score = ssc;
+  *input = bin;
+  *steps = bst;
+  *n_tokens = 0;
+  if (bin < 0 || sst == SLOT_EMPTY) return SB_OK;
+  // Tokens: walk this input's backpointers from level `steps`.
+  std::vector<uint32_t> bp((size_t)st.max_len_cap * st.k);
+  HIPCHK(hipMemcpyAsync(bp.data(), st.bp + (size_t)bin * st.max_len_cap * st.k, bp.size() * 4,
+                        hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  std::vector<int32_t> rev;
+  int pos = rank;
+  for (int lev = bst; lev >= 1; --lev) {
+    const uint32_t e = bp[(size_t)(lev - 1) * st.k + pos];
+    if ((e & 0xFFFFFFu) != BP_NOOP) rev.push_back((int32_t)(e & 0xFFFFFFu));
+    pos = (int)(e >> 24);
+  }
+  *n_tokens = (int32_t)rev.size();
+  if (tokens)
+    for (int i = 0; i < (int)rev.size() && i < tok_cap; ++i) tokens[i] = rev[rev.size() - 1 - i];
+  if (kv && st.kv_layers > 0 && sst == SLOT_ACTIVE) {
+    const int planes = st.kv_layers * 2;
+    const size_t plane_elems = (size_t)st.max_len_cap * st.d;
+    const uint16_t *buf = bpar ? st.kv1 : st.kv0;
+    for (int pl = 0; pl < planes; ++pl) {
+      const int64_t need = (int64_t)(pl + 1) * bst * st.d;
+      if (need > kv_cap) break;
+      HIPCHK(hipMemcpyAsync(kv + (size_t)pl * bst * st.d, buf + ((size_t)slot * planes + pl) * plane_elems,
+                            (size_t)bst * st.d * 2, hipMemcpyDeviceToHost, dec->stream));
+    }
+    HIPCHK(hipStreamSynchronize(dec->stream));
+  }
+  return SB_OK;
+}
+
+sb_status sb_destroy(sb_decoder *dec) {
+  if (!dec) return SB_E_INVALID_ARG;
+  (void)hipStreamSynchronize(dec->stream);
+  for (auto e : dec->tev)
+    if (e) (void)hipEventDestroy(e);
+  for (int i = 0; i < 2; ++i)
+    if (dec->poll_ev[i]) (void)hipEventDestroy(dec->poll_ev[i]);
+  if (dec->pinned_len) (void)hipHostFree(dec->pinned_len);
+  if (dec->pinned_flag) (void)hipHostFree(dec->pinned_flag);
+  delete dec;
+  return SB_OK;
+}
+
+}  // extern "C"

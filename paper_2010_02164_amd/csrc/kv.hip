@@ -1,0 +1,162 @@
+// Per-candidate KV-like state: every expansion appends the rows
+// bf16(h . W_kv[l][j]) (l < L layers, j in {K, V}) at position l_t - 1, and
+// every beam update hands each surviving active candidate a copy of its
+// parent's rows (the reorder of incremental decoder state that the paper's
+// transformer decoder performs, App. A.2). State lives in two buffers; a
+// beam's rows move to the other buffer at each of its steps, so a parent's
+// rows are never overwritten while a child still needs them.
+#include "sb_internal.h"
+
+namespace sb {
+namespace {
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+
+constexpr int THREADS = 256;
+constexpr int BV = GEMM_BV, BR = GEMM_BR;
+constexpr int ROWB = 128, LSTRIDE = ROWB + 16;
+
+struct Smem {
+  unsigned char A[2][BV][LSTRIDE];
+  unsigned char B[2][BR][LSTRIDE];
+};
+
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// kvnew[r][o] = bf16(sum_i h[r][i] * W_kvT[o][i]), o over L*2*d outputs.
+__global__ __launch_bounds__(THREADS, 2) void k_kv_append(DevState st) {
+  const int R = st.ctrl->R;
+  const int d = st.d, NO = st.kv_layers * 2 * d;
+  const int nvt = NO / BV, nrt = (st.R_max + BR - 1) / BR;
+  const int g = blockIdx.x;
+  const int vt = g / nrt, rt = g - vt * nrt;
+  const int v0 = vt * BV, r0 = rt * BR;
+  if (r0 >= R) return;
+  __shared__ Smem sm;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wv = w & 1, wb = w >> 1;
+  const int rowbytes = d * 2;
+  const int row0 = tid >> 3, col = tid & 7;
+  const unsigned char *ap[4], *bp[2];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    ap[u] = reinterpret_cast<const unsigned char *>(st.wkvT) + (size_t)(v0 + row0 + 32 * u) * rowbytes + col * 16;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+    bp[u] = static_cast<const unsigned char *>(st.hbuf) + (size_t)min(r0 + row0 + 32 * u, R - 1) * rowbytes + col * 16;
+  u4 ra[4], rb[2];
+  auto load = [&](int kt) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) ra[u] = *reinterpret_cast<const u4 *>(ap[u] + kt * ROWB);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) rb[u] = *reinterpret_cast<const u4 *>(bp[u] + kt * ROWB);
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) *reinterpret_cast<u4 *>(&sm.A[buf][row0 + 32 * u][col * 16]) = ra[u];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) *reinterpret_cast<u4 *>(&sm.B[buf][row0 + 32 * u][col * 16]) = rb[u];
+  };
+  f16v acc0 = {}, acc1 = {};
+  const int nk = rowbytes / ROWB;
+  load(0);
+  store(0);
+  __syncthreads();
+  const int r = lane & 31, h = (lane >> 5) * 16;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) load(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int off = ks * 32 + h;
+      const bf8 a0 = *reinterpret_cast<const bf8 *>(&sm.A[cur][wv * 64 + r][off]);
+      const bf8 a1 = *reinterpret_cast<const bf8 *>(&sm.A[cur][wv * 64 + 32 + r][off]);
+      const bf8 b0 = *reinterpret_cast<const bf8 *>(&sm.B[cur][wb * 32 + r][off]);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc1, 0, 0, 0);
+    }
+    if (kt + 1 < nk) store(cur ^ 1);
+    __syncthreads();
+  }
+  const int j = r0 + wb * 32 + (lane & 31);
+  if (j >= R) return;
+  uint16_t *out = st.kvnew + (size_t)j * NO;
+#pragma unroll
+  for (int vb = 0; vb < 2; ++vb) {
+    const f16v &acc = vb ? acc1 : acc0;
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int o = v0 + wv * 64 + vb * 32 + 8 * gq + 4 * (lane >> 5);
+      u2 pk;
+      pk[0] = (uint32_t)bf16_rne(acc[4 * gq + 0]) | ((uint32_t)bf16_rne(acc[4 * gq + 1]) << 16);
+      pk[1] = (uint32_t)bf16_rne(acc[4 * gq + 2]) | ((uint32_t)bf16_rne(acc[4 * gq + 3]) << 16);
+      *reinterpret_cast<u2 *>(out + o) = pk;
+    }
+  }
+}
+
+// One workgroup per (slot, plane): if the slot holds an active candidate
+// created this step, copy its parent's rows 0..t-2 from the old buffer and
+// write row t-1 from kvnew of the parent's row.
+__global__ __launch_bounds__(THREADS) void k_kv_gather(DevState st) {
+  if (st.ctrl->R == 0) return;
+  const int planes = st.kv_layers * 2;
+  const int slot = blockIdx.x / planes;
+  const int plane = blockIdx.x - slot * planes;
+  const int b = slot / st.k;
+  if (!st.b_sel[b] || st.b_input[b] < 0) return;   // not stepped, or finished
+  const int prow = st.s_prow[slot];
+  if (prow < 0) return;
+  const int src_slot = st.r_slot[prow];
+  const int t = st.b_steps[b];                     // rows after this step
+  const int par = st.b_par[b];                     // buffer holding the new rows
+  uint16_t *dstbuf = par ? st.kv1 : st.kv0;
+  const uint16_t *srcbuf = par ? st.kv0 : st.kv1;
+  const size_t plane_elems = (size_t)st.max_len_cap * st.d;
+  const size_t slot_elems = plane_elems * planes;
+  const u4 *src = reinterpret_cast<const u4 *>(srcbuf + src_slot * slot_elems + plane * plane_elems);
+  u4 *dst = reinterpret_cast<u4 *>(dstbuf + (size_t)slot * slot_elems + plane * plane_elems);
+  const int row_chunks = st.d / 8;                 // 16-byte chunks per row
+  const int copy_chunks = (t - 1) * row_chunks;
+  for (int c = threadIdx.x; c < copy_chunks; c += THREADS) dst[c] = src[c];
+  const u4 *nw = reinterpret_cast<const u4 *>(st.kvnew + (size_t)prow * planes * st.d + (size_t)plane * st.d);
+  for (int c = threadIdx.x; c < row_chunks; c += THREADS) dst[copy_chunks + c] = nw[c];
+}
+
+__global__ void k_transpose(const uint16_t *W, uint16_t *WT, int L2, int d) {
+  // W [L2][d_in][d_out] -> WT [L2][d_out][d_in]
+  const size_t total = (size_t)L2 * d * d;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (size_t)gridDim.x * blockDim.x) {
+    const size_t p = e / ((size_t)d * d);
+    const size_t rem = e - p * d * d;
+    const size_t i = rem / d, o = rem - i * d;
+    WT[p * d * d + o * d + i] = W[e];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kv_append(const DevState &st, hipStream_t s) {
+  const int NO = st.kv_layers * 2 * st.d;
+  const int G = (NO / BV) * ((st.R_max + BR - 1) / BR);
+  hipLaunchKernelGGL(k_kv_append, dim3(G), dim3(THREADS), 0, s, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_gather(const DevState &st, hipStream_t s) {
+  const int G = st.n * st.k * st.kv_layers * 2;
+  hipLaunchKernelGGL(k_kv_gather, dim3(G), dim3(THREADS), 0, s, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s) {
+  hipLaunchKernelGGL(k_transpose, dim3(1024), dim3(256), 0, s, W_kv, st.wkvT, st.kv_layers * 2, st.d);
+  return hipGetLastError();
+}
+
+}  // namespace sb

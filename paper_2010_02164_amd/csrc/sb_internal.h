@@ -1,0 +1,103 @@
+// Internal device-state layout and kernel launchers of the streambeam library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sb {
+
+enum : int32_t { SLOT_EMPTY = 0, SLOT_ACTIVE = 1, SLOT_EOS = 2, SLOT_MAXLEN = 3 };
+
+// Backpointer entry of the per-beam history table: parent rank in the
+// previous beam (bits 24..31) and the emitted token (bits 0..23); a no-op
+// expansion of a terminated candidate stores BP_NOOP as its token.
+constexpr uint32_t BP_NOOP = 0xFFFFFFu;
+constexpr int KMAX_SUPPORTED = 16;
+
+// Device-side control block: the scheduler state of Alg. 1 and the counters.
+struct DevCtrl {
+  int32_t n_queued;   // inputs submitted so far
+  int32_t cursor;     // next input to admit (Alg. 1's c)
+  int32_t R;          // rows (active candidates) expanded this step
+  int32_t t_sel;      // 1-based index of the token the selected beams emit
+  int32_t live;       // live beams after admission
+  int32_t done;       // 1: nothing queued and no beam live
+  int32_t n_sel;      // beams selected this step
+  int32_t pad0;
+  int64_t timesteps, expansions, noops, refills, admitted, hyps, finished;
+};
+
+// A finalized hypothesis. The beam kernel records where its history ends
+// (level = steps taken, rank = position in the final beam); the backtrack
+// kernel later walks the backpointers to fill `length` and the tokens.
+struct OutHyp {
+  double score;
+  int32_t length, status, finalize_step, level;
+};
+
+// All device pointers and sizes a kernel may need, passed by value.
+struct DevState {
+  DevCtrl *ctrl;
+  // input queue
+  void *q_h0;          // [max_inputs][d]
+  int32_t *q_Lx, *q_ml;
+  // beams [n]
+  int32_t *b_input;    // queue position, -1 = free
+  int32_t *b_steps;    // l_t: steps taken
+  int32_t *b_sel;      // 1 if expanded this step
+  int32_t *b_par;      // which KV buffer holds this beam's state
+  // candidate slots [n*k], slot = beam*k + rank
+  int32_t *s_status;
+  double *s_score;
+  int32_t *s_tok;      // last token (0 for a fresh beam: the start symbol)
+  void *s_h;           // [n*k][d] state after consuming the candidate's tokens
+  int32_t *s_row;      // row of the slot this step, -1 if not expanded
+  int32_t *s_prow;     // for the KV gather: row of the new candidate's parent, -1 if none
+  uint32_t *bp;        // [max_inputs][max_len_cap][k] backpointers, by queue position
+  // rows [R_max]: per-row metadata written by the scheduler
+  int32_t *r_slot;     // slot of the expanded candidate
+  int32_t *r_hsrc;     // state source: >= 0 slot index into s_h, < 0 queue row (-1 - q) of q_h0
+  int32_t *r_y;        // last token, consumed by the recurrence
+  int32_t *r_t;        // 1-based index of the token being emitted (EOS bias, max length)
+  int32_t *r_Lx;       // L_x of the row's input (EOS bias)
+  double *r_lse;       // log-sum-exp of the row's logits
+  void *hbuf;          // [R_max][d] new states of the expanded rows
+  float *part;         // [R_max][S][2 + 2k] per-tile (max, sumexp, top-k vals, top-k ids)
+  double *top_lp;      // [R_max][k] log-probs of each row's best k tokens
+  int32_t *top_tok;    // [R_max][k]
+  // outputs, indexed by queue position
+  int32_t *o_count;    // [max_inputs] |Y[i]| (0 = unfinished)
+  OutHyp *o_hyp;       // [max_inputs][k]
+  int32_t *o_tok;      // [max_inputs][k][max_len_cap]
+  // KV-like state (bf16 bits)
+  uint16_t *kv0, *kv1; // [n*k][L][2][max_len_cap][d]
+  uint16_t *kvnew;     // [R_max][L*2*d]
+  uint16_t *wkvT;      // [L*2*d][d]  (transposed W_kv: out-feature major)
+  // model
+  const void *W_h, *E, *W_out;
+  // sizes and parameters
+  int32_t n, k, d, V, M, max_len_cap, refill_thr, S, R_max, dtype, kv_layers, max_inputs;
+  int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
+  double delta;
+  float beta;
+};
+
+// Tile sizes of the projection/recurrence GEMMs.
+constexpr int GEMM_BV = 128;   // out features (vocab / hidden) per workgroup
+constexpr int GEMM_BR = 64;    // batch rows per workgroup
+
+inline int proj_tiles(int V) { return (V + GEMM_BV - 1) / GEMM_BV; }
+
+// Launchers (each returns the launch status).
+hipError_t launch_sched(const DevState &st, hipStream_t s);
+hipError_t launch_rec(const DevState &st, hipStream_t s);
+hipError_t launch_proj(const DevState &st, hipStream_t s);
+hipError_t launch_rowmerge(const DevState &st, hipStream_t s);
+hipError_t launch_beam(const DevState &st, hipStream_t s);
+hipError_t launch_kv_append(const DevState &st, hipStream_t s);
+hipError_t launch_kv_gather(const DevState &st, hipStream_t s);
+hipError_t launch_backtrack(const DevState &st, int q0, int q1, hipStream_t s);
+hipError_t launch_init(const DevState &st, hipStream_t s);
+hipError_t launch_transpose_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s);
+
+}  // namespace sb

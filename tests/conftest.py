@@ -9,3 +9,24 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+import pytest  # noqa: E402
+
+
+@pytest.fixture(scope="session")
+def native_lib():
+    """The built HIP library (built in-tree first if it is missing)."""
+    from paper_2010_02164_amd import _native
+    if not os.path.exists(_native.LIB_PATH):
+        from paper_2010_02164_amd import build
+        build.build()
+    return _native.lib()
+
+
+@pytest.fixture(scope="session")
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")

@@ -1,0 +1,49 @@
+"""Helpers shared by the GPU tests: run the HIP search on a workload and
+compare it with the oracle."""
+import math
+
+import numpy as np
+
+from oracle.compare import compare
+from oracle.search import decode_workload
+
+
+def gpu_decode(wl, sched, eps=None, n=None, inputs=None, weights=None, timing=False):
+    """Run the HIP decoder over (a subset of) a workload; returns
+    (per-input hypotheses, stats, decoder)."""
+    import torch
+    from paper_2010_02164_amd import decoder_for_workload, group_by_input, inputs_to_device
+    idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
+    dec = decoder_for_workload(wl, sched=sched, eps=eps, n=n, max_inputs=len(idx), weights=weights)
+    if timing:
+        dec.set_timing(True)
+    dec.submit(inputs_to_device(wl, idx), wl.Lx[idx], wl.max_len[idx])
+    dec.run()
+    hyps = group_by_input(dec.collect(), len(idx))
+    st = dec.stats()
+    torch.cuda.synchronize()
+    return hyps, st, dec
+
+
+def score_tol(wl):
+    return 2e-2 if wl.is_bf16 else 1e-4
+
+
+def check_parity(wl, sched, eps=None, n=None, inputs=None, oracle_res=None, weights=None,
+                 require_stats=True):
+    """GPU vs oracle on the same inputs; returns the comparison report."""
+    idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
+    o = oracle_res or decode_workload(wl, sched=sched, eps=eps, n=n, inputs=idx)
+    g, st, dec = gpu_decode(wl, sched, eps=eps, n=n, inputs=idx, weights=weights)
+    dec.close()
+    rep = compare(o.hyps, o.min_margin, [[(h.tokens, h.score, h.status) for h in y] for y in g],
+                  inputs=idx, score_tol=score_tol(wl))
+    print(f"[parity] {wl.cfg.name} {sched} eps={eps} n={n} N={len(idx)}: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures[:5]
+    if require_stats and rep.n_excused == 0:
+        for key in ("timesteps", "expansions", "noops", "refills", "admitted"):
+            assert st[key] == getattr(o, key), (key, st[key], getattr(o, key))
+        assert st["hyps"] == o.n_hyps
+        fin = [y[0].finalize_step for y in g]
+        assert fin == list(o.finalize_step)
+    return rep, g, st, o
