@@ -1,0 +1,145 @@
+"""Benchmark of the streaming beam-search decoder on one MI355X.
+
+A bench "step" is one whole decode of the workload: queue every input
+(device-resident encodings), run the search until every beam is finished
+(refill, selection, expansion, top-k, pruning, finalization, state reorder,
+and the rebuild of the output tokens, all in device memory). Output copies
+to the host are outside the timed region and reported separately.
+
+Default workload: the MT-shaped fp32 configuration (N=4096 inputs, n=128,
+k=5, |V|=32000, d=1024, Var-Stream eps=1/4, delta=1.5), synthetic.
+
+Prints one JSON line: finalized hypotheses/s (value), candidate
+expansions/s, the projection kernel's achieved MFMA rate against the
+MI355X peak (timed with HIP events on the decoder's stream), and the fp64
+oracle timed on this host's cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA, MI355X
+METRIC = "finalized hyps/sec + expansions/sec (Var-Stream, k=5, |V|=32k), % roofline"
+
+
+def _workload_desc(cfg, sched, eps):
+    return (f"{cfg.name}: N={cfg.N} inputs, n={cfg.n}, k={cfg.k}, |V|={cfg.V}, d={cfg.d}, "
+            f"{cfg.dtype}, {sched} eps={eps:g}, delta={cfg.delta:g}, M={cfg.M}, "
+            f"L_x {cfg.lengths}[{cfg.len_lo},{cfg.len_hi}]"
+            + (f", KV {cfg.kv_layers}x2xtxd" if cfg.kv_layers else ""))
+
+
+def cpu_baseline(wl, sched, eps, sample):
+    """The fp64 oracle (as it stands) on the first `sample` inputs."""
+    from oracle.search import decode_workload
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 0) for i in threadpool_info()] or [0])
+    except Exception:
+        threads = 0
+    cores = threads or len(os.sched_getaffinity(0))
+    idx = np.arange(min(sample, len(wl.Lx)))
+    t0 = time.perf_counter()
+    r = decode_workload(wl, sched=sched, eps=eps, inputs=idx)
+    dt = time.perf_counter() - t0
+    return {"value": r.n_hyps / dt, "unit": "hyps/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {len(idx)} of {len(wl.Lx)} inputs, same n/k/eps/delta/M, numpy fp64 "
+                      f"({dt:.1f} s, {r.expansions} expansions)",
+            "expansions_per_s": r.expansions / dt, "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--sched", default="var_stream", choices=["fixed", "var_batch", "var_stream"])
+    ap.add_argument("--eps", type=float, default=None)
+    ap.add_argument("--cpu-sample", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(inputs are independent: shard them over GPUs, one decoder per GPU)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2010_02164_amd import decoder_for_workload, inputs_to_device, weights_to_device
+    from synthgen import get_config, make_workload
+
+    cfg = get_config(args.config)
+    eps = cfg.eps if args.eps is None else args.eps
+    if args.sched != "var_stream":
+        eps = 0.0
+    wl = make_workload(cfg)
+    weights = weights_to_device(wl)
+    h0 = inputs_to_device(wl)
+    dec = decoder_for_workload(wl, sched=args.sched, eps=eps, weights=weights)
+    N = len(wl.Lx)
+
+    def run_once():
+        dec.reset()
+        dec.submit(h0, wl.Lx, wl.max_len)
+        dec.run()
+
+    for _ in range(args.warmup):
+        run_once()
+    torch.cuda.synchronize()
+    dec.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_once()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    proj_ms, proj_launches = dec.timing()
+    dec.set_timing(False)
+    st = dec.stats()            # counters of the last run
+    t1 = time.perf_counter()
+    hyps = dec.collect()
+    collect_s = time.perf_counter() - t1
+    assert len(hyps) == st["hyps"]
+
+    per_run = elapsed / args.steps
+    hyps_per_s = st["hyps"] / per_run
+    exps_per_s = st["expansions"] / per_run
+    # Projection: 2 d |V| flops per expansion (algorithmic), every timed run.
+    proj_flops = 2.0 * cfg.d * cfg.V * st["expansions"] * args.steps
+    achieved = proj_flops / (proj_ms * 1e-3) / 1e12 if proj_ms > 0 else 0.0
+    peak = PEAK_TFLOPS[cfg.dtype]
+    out = {
+        "metric": METRIC, "value": hyps_per_s, "unit": "hyps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": per_run * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": _workload_desc(cfg, args.sched, eps), "inputs": N,
+                   "parallelism": "single GPU"},
+        "expansions_per_s": exps_per_s,
+        "search": {k: st[k] for k in ("timesteps", "expansions", "noops", "refills", "hyps")},
+        "roofline": {"bound": "mfma", "kernel": "k_proj (vocabulary projection + log-sum-exp + top-k)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": None, "launches": proj_launches,
+                     "avg_launch_us": proj_ms * 1e3 / max(proj_launches, 1)},
+        "projection_share_of_step": (proj_ms * 1e-3) / elapsed if elapsed > 0 else None,
+        "collect_d2h_ms": collect_s * 1e3,
+        "pcie_inclusive_hyps_per_s": st["hyps"] / (per_run + collect_s),
+    }
+    dec.close()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.sched, eps, args.cpu_sample)
+        out["gpu_over_cpu"] = hyps_per_s / out["cpu_baseline"]["value"]
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -141,7 +141,8 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_
  * is pending and no beam is live, else 0. With done == NULL nothing waits. */
 sb_status sb_step(sb_decoder *dec, int32_t *done);
 
-/* Step until every submitted input is finished; returns after the stream has
+/* Step until every submitted input is finished, then rebuild the tokens of
+ * every finished hypothesis in device memory; returns after the stream has
  * completed the work. */
 sb_status sb_run(sb_decoder *dec);
 

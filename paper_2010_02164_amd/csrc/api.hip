@@ -396,6 +396,8 @@ sb_status sb_run(sb_decoder *dec) {
       return SB_E_STATE;
     }
   }
+  // Rebuild the tokens of every finished hypothesis in device memory.
+  HIPCHK(launch_backtrack(dec->st, dec->collected, dec->n_queued, dec->stream));
   HIPCHK(hipStreamSynchronize(dec->stream));
   return SB_OK;
 }

@@ -75,9 +75,11 @@ __device__ __forceinline__ bool cand_beats(double sa, int pa, int ta, double sb,
   return ta < tb;
 }
 
-__global__ __launch_bounds__(64) void k_beam(DevState st) {
+constexpr int BEAM_THREADS = 256;
+
+__global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x;   // 0..255
   if (st.ctrl->R == 0 || !st.b_sel[b]) return;
   const int k = st.k;
   const int base = b * k;
@@ -99,7 +101,7 @@ __global__ __launch_bounds__(64) void k_beam(DevState st) {
   if (lane == 0) nvalid_sh = 0;
   if (lane < KMAX_SUPPORTED) at_rank[lane] = -1;
   __syncthreads();
-  for (int q = lane; q < C; q += 64) {
+  for (int q = lane; q < C; q += BEAM_THREADS) {
     int valid = 0, par, tok = -1;
     double sc = 0.0;
     if (q < k * k) {
@@ -128,7 +130,7 @@ __global__ __launch_bounds__(64) void k_beam(DevState st) {
   __syncthreads();
 
   // Full beam B': rank of every valid candidate among the valid ones.
-  for (int q = lane; q < C; q += 64) {
+  for (int q = lane; q < C; q += BEAM_THREADS) {
     if (!cv[q]) continue;
     int rank = 0;
     for (int o = 0; o < C; ++o)
@@ -221,14 +223,23 @@ __global__ __launch_bounds__(64) void k_beam(DevState st) {
     st.b_par[b] ^= 1;
   }
   // State copy: s_h[rank] <- hbuf[row(parent)] for every active survivor.
+  // All survivors' loads are issued before any store (up to k rows in flight).
   const int rowbytes = st.d * (st.dtype == 1 ? 2 : 4);
   const int chunks = rowbytes / 16;
-  for (int r = 0; r < w; ++r) {
-    if (nstat[r] != SLOT_ACTIVE) continue;
-    const int prow = st.s_row[base + npar[r]];
-    const uint4 *src = reinterpret_cast<const uint4 *>(static_cast<const unsigned char *>(st.hbuf) + (size_t)prow * rowbytes);
-    uint4 *dst = reinterpret_cast<uint4 *>(static_cast<unsigned char *>(st.s_h) + (size_t)(base + r) * rowbytes);
-    for (int c = lane; c < chunks; c += 64) dst[c] = src[c];
+  int prow[KMAX_SUPPORTED];
+#pragma unroll
+  for (int r = 0; r < KMAX_SUPPORTED; ++r)
+    prow[r] = (r < w && nstat[r] == SLOT_ACTIVE) ? st.s_row[base + npar[r]] : -1;
+  const unsigned char *hb = static_cast<const unsigned char *>(st.hbuf);
+  unsigned char *sh = static_cast<unsigned char *>(st.s_h);
+  for (int c = lane; c < chunks; c += BEAM_THREADS) {
+    uint4 v[KMAX_SUPPORTED];
+#pragma unroll
+    for (int r = 0; r < KMAX_SUPPORTED; ++r)
+      if (prow[r] >= 0) v[r] = reinterpret_cast<const uint4 *>(hb + (size_t)prow[r] * rowbytes)[c];
+#pragma unroll
+    for (int r = 0; r < KMAX_SUPPORTED; ++r)
+      if (prow[r] >= 0) reinterpret_cast<uint4 *>(sh + (size_t)(base + r) * rowbytes)[c] = v[r];
   }
 }
 
@@ -275,7 +286,7 @@ hipError_t launch_rowmerge(const DevState &st, hipStream_t s) {
 }
 
 hipError_t launch_beam(const DevState &st, hipStream_t s) {
-  hipLaunchKernelGGL(k_beam, dim3(st.n), dim3(64), 0, s, st);
+  hipLaunchKernelGGL(k_beam, dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
   return hipGetLastError();
 }
 

@@ -173,134 +173,147 @@ __device__ __forceinline__ uint16_t bf16_rne_from_double(double x) {
   return (uint16_t)(__float_as_uint(f) >> 16);
 }
 
-// ---------------------------------------------------------------- K_rec f32
-__global__ __launch_bounds__(THREADS, 2) void k_rec_f32(DevState st) {
-  const int R = st.ctrl->R;
-  const int d = st.d;
-  const int nvt = (d + BV - 1) / BV, nrt = (st.R_max + BR - 1) / BR;
-  int vt, rt;
-  tile_of(nvt, nrt, vt, rt);
-  const int v0 = vt * BV, r0 = rt * BR;
-  if (r0 >= R) return;
-  __shared__ Smem sm;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wv = w & 1, wb = w >> 1;
-  const int rowbytes = d * 4;
-  Stager sg;
-  setup_stager(sg, st, st.W_h, d, v0, r0, R, rowbytes, nullptr);
-  f16v acc0 = {}, acc1 = {};
-  gemm_mainloop<false>(sm, sg, rowbytes / ROWB, wv, wb, lane, acc0, acc1);
+// ---------------------------------------------------------------- K_rec
+// The recurrence GEMM is small ([R,d] x [d,d]) next to the projection, so it
+// is cut into 32 (out features) x 32 (rows) tiles to reach hundreds of
+// workgroups, and the K loop of each tile is split over the 4 waves of the
+// workgroup; the 4 partial sums are added in a fixed order (wave 0 + 1 + 2
+// + 3), so the result does not depend on which rows share the step. Operands
+// are read straight from global memory (W_h and the states are L2/MALL
+// resident); each lane loads the 16 bytes it feeds to the MFMA.
+constexpr int RT = 32;        // tile edge
+constexpr int RSPLIT = 4;     // K split over the waves
 
-  // Epilogue: lane holds out features i = base + 8*(reg/4) + 4*(lane/32) +
-  // reg%4 of batch row j = r0 + wb*32 + lane%32.
-  const int j = r0 + wb * 32 + (lane & 31);
-  if (j >= R) return;
-  const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[j] * d;
-  float *out = static_cast<float *>(st.hbuf) + (size_t)j * d;
-#pragma unroll
-  for (int vb = 0; vb < 2; ++vb) {
-    const f16v &acc = vb ? acc1 : acc0;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int i = v0 + wv * 64 + vb * 32 + 8 * g + 4 * (lane >> 5);
-      if (i < d) {
-        const f4 e = *reinterpret_cast<const f4 *>(E + i);
-        f4 hv;
-        hv[0] = tanhf(acc[4 * g + 0] + e[0]);
-        hv[1] = tanhf(acc[4 * g + 1] + e[1]);
-        hv[2] = tanhf(acc[4 * g + 2] + e[2]);
-        hv[3] = tanhf(acc[4 * g + 3] + e[3]);
-        *reinterpret_cast<f4 *>(out + i) = hv;
-      }
-    }
-  }
+__device__ __forceinline__ const unsigned char *rec_state_row(const DevState &st, int r, int R, int rowbytes) {
+  return state_row(st, min(r, R - 1), rowbytes);
 }
 
-// ------------------------------------------------------- K_rec bf16 (fp64)
+__global__ __launch_bounds__(THREADS) void k_rec_f32(DevState st) {
+  const int R = st.ctrl->R;
+  const int d = st.d;
+  const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
+  int vt, rt;
+  tile_of(nvt, nrt, vt, rt);
+  const int v0 = vt * RT, r0 = rt * RT;
+  if (r0 >= R) return;
+  __shared__ float red[RSPLIT][RT * RT];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rowbytes = d * 4;
+  const int kq = d / RSPLIT;                       // K range of this wave
+  const float *arow = static_cast<const float *>(st.W_h) + (size_t)(v0 + (lane & 31)) * d + w * kq;
+  const float *brow = reinterpret_cast<const float *>(rec_state_row(st, r0 + (lane & 31), R, rowbytes)) + w * kq;
+  const int h = (lane >> 5) * 4;
+  f16v acc = {};
+#pragma unroll 4
+  for (int kk = 0; kk < kq; kk += 8) {
+    const f4 a = *reinterpret_cast<const f4 *>(arow + kk + h);
+    const f4 b = *reinterpret_cast<const f4 *>(brow + kk + h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc, 0, 0, 0);
+  }
+  // acc: out feature i = 8*(reg/4) + 4*(lane/32) + reg%4, row j = lane%32.
+#pragma unroll
+  for (int reg = 0; reg < 16; ++reg) {
+    const int i = 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
+    red[w][(lane & 31) * RT + i] = acc[reg];
+  }
+  __syncthreads();
+  // 256 threads x 4 outputs: thread -> row j = tid/8, features 4*(tid%8)..+3.
+  const int j = threadIdx.x >> 3, i0 = (threadIdx.x & 7) * 4;
+  const int row = r0 + j;
+  if (row >= R) return;
+  const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+  const f4 e = *reinterpret_cast<const f4 *>(E);
+  f4 hv;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int o = j * RT + i0 + q;
+    const float pre = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
+    hv[q] = tanhf(pre + e[q]);
+  }
+  *reinterpret_cast<f4 *>(static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0) = hv;
+}
+
 // bf16 states are rounded after tanh, a discontinuous map: any difference
 // in the pre-activation can flip a rounding and then grows step after step.
 // Products of two bf16 values are exact in fp64 and so is their sum over
 // the state size in practice, so the pre-activation is accumulated with the
-// fp64 MFMA, tanh taken in fp64 and the result rounded once to bf16.
-__global__ __launch_bounds__(THREADS, 2) void k_rec_bf16(DevState st) {
+// fp64 MFMA (16x16x4), tanh taken in fp64 and the result rounded once.
+__global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
   const int R = st.ctrl->R;
   const int d = st.d;
-  const int nvt = (d + BV - 1) / BV, nrt = (st.R_max + BR - 1) / BR;
+  const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
   int vt, rt;
   tile_of(nvt, nrt, vt, rt);
-  const int v0 = vt * BV, r0 = rt * BR;
+  const int v0 = vt * RT, r0 = rt * RT;
   if (r0 >= R) return;
-  __shared__ Smem sm;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wv = w & 1, wb = w >> 1;
+  __shared__ double red[RSPLIT][RT * RT];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rowbytes = d * 2;
-  Stager sg;
-  setup_stager(sg, st, st.W_h, d, v0, r0, R, rowbytes, nullptr);
-  // Wave sub-tile: 64 out features (4 blocks of 16) x 32 rows (2 blocks of 16).
-  d4 acc[4][2];
+  const int kq = d / RSPLIT;
+  const int r16 = lane & 15, g = lane >> 4;
+  // A: 2 blocks of 16 out features, B: 2 blocks of 16 rows; the lane feeds
+  // 4 consecutive bf16 at k = kk + 4g to 4 MFMAs (same permutation for A, B).
+  const uint16_t *a0 = static_cast<const uint16_t *>(st.W_h) + (size_t)(v0 + r16) * d + w * kq + 4 * g;
+  const uint16_t *a1 = a0 + (size_t)16 * d;
+  const uint16_t *b0 = reinterpret_cast<const uint16_t *>(rec_state_row(st, r0 + r16, R, rowbytes)) + w * kq + 4 * g;
+  const uint16_t *b1 = reinterpret_cast<const uint16_t *>(rec_state_row(st, r0 + 16 + r16, R, rowbytes)) + w * kq + 4 * g;
+  d4 acc[2][2];
 #pragma unroll
-  for (int ib = 0; ib < 4; ++ib)
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int jb = 0; jb < 2; ++jb) acc[ib][jb] = d4{0.0, 0.0, 0.0, 0.0};
-
-  const int nk = rowbytes / ROWB;
-  sg.load(0);
-  sg.store(sm, 0);
-  __syncthreads();
-  const int r16 = lane & 15;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) sg.load(kt + 1);
+    for (int y = 0; y < 2; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+  auto cvt = [](u2 raw, double *o) {
+    o[0] = (double)__uint_as_float(raw[0] << 16);
+    o[1] = (double)__uint_as_float(raw[0] & 0xFFFF0000u);
+    o[2] = (double)__uint_as_float(raw[1] << 16);
+    o[3] = (double)__uint_as_float(raw[1] & 0xFFFF0000u);
+  };
+#pragma unroll 2
+  for (int kk = 0; kk < kq; kk += 16) {
+    double a[2][4], b[2][4];
+    cvt(*reinterpret_cast<const u2 *>(a0 + kk), a[0]);
+    cvt(*reinterpret_cast<const u2 *>(a1 + kk), a[1]);
+    cvt(*reinterpret_cast<const u2 *>(b0 + kk), b[0]);
+    cvt(*reinterpret_cast<const u2 *>(b1 + kk), b[1]);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      // 16x16x4 f64 with a K permutation: the lane's 4 consecutive bf16 at
-      // k = 16ks + 4*(lane/16) feed 4 MFMAs, identically for A and B.
-      const int off = ks * 32 + (lane >> 4) * 8;
-      double a[4][4], b[2][4];
+    for (int e = 0; e < 4; ++e)
 #pragma unroll
-      for (int ib = 0; ib < 4; ++ib) {
-        const u2 raw = *reinterpret_cast<const u2 *>(&sm.A[cur][wv * 64 + ib * 16 + r16][off]);
-        a[ib][0] = (double)__uint_as_float(raw[0] << 16);
-        a[ib][1] = (double)__uint_as_float(raw[0] & 0xFFFF0000u);
-        a[ib][2] = (double)__uint_as_float(raw[1] << 16);
-        a[ib][3] = (double)__uint_as_float(raw[1] & 0xFFFF0000u);
-      }
+      for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int jb = 0; jb < 2; ++jb) {
-        const u2 raw = *reinterpret_cast<const u2 *>(&sm.B[cur][wb * 32 + jb * 16 + r16][off]);
-        b[jb][0] = (double)__uint_as_float(raw[0] << 16);
-        b[jb][1] = (double)__uint_as_float(raw[0] & 0xFFFF0000u);
-        b[jb][2] = (double)__uint_as_float(raw[1] << 16);
-        b[jb][3] = (double)__uint_as_float(raw[1] & 0xFFFF0000u);
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-#pragma unroll
-        for (int ib = 0; ib < 4; ++ib)
-#pragma unroll
-          for (int jb = 0; jb < 2; ++jb)
-            acc[ib][jb] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[ib][e], b[jb][e], acc[ib][jb], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sg.store(sm, cur ^ 1);
-    __syncthreads();
+        for (int y = 0; y < 2; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x][e], b[y][e], acc[x][y], 0, 0, 0);
   }
-
-  // Epilogue: the f64 16x16x4 result block (ib, jb) holds, in lane l and
-  // register q, out feature i = (l/16) + 4q of the block and batch column
-  // j = l%16.
+  // f64 16x16x4 result: lane l, register q hold out feature (l/16) + 4q of
+  // the block and row l%16.
 #pragma unroll
-  for (int jb = 0; jb < 2; ++jb) {
-    const int j = r0 + wb * 32 + jb * 16 + r16;
-    if (j >= R) continue;
-    const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[j] * d;
-    uint16_t *out = static_cast<uint16_t *>(st.hbuf) + (size_t)j * d;
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
+    for (int y = 0; y < 2; ++y)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int i = v0 + wv * 64 + ib * 16 + (lane >> 4) + 4 * q;
-        if (i < d) out[i] = bf16_rne_from_double(tanh(acc[ib][jb][q] + (double)bf16f(E[i])));
+        const int i = x * 16 + g + 4 * q, j = y * 16 + r16;
+        red[w][j * RT + i] = acc[x][y][q];
       }
-    }
+  __syncthreads();
+  const int j = threadIdx.x >> 3, i0 = (threadIdx.x & 7) * 4;
+  const int row = r0 + j;
+  if (row >= R) return;
+  const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+  const u2 eraw = *reinterpret_cast<const u2 *>(E);
+  double e[4];
+  cvt(eraw, e);
+  uint16_t hb[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int o = j * RT + i0 + q;
+    const double pre = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
+    hb[q] = bf16_rne_from_double(tanh(pre + e[q]));
   }
+  u2 packed;
+  packed[0] = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+  packed[1] = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
+  *reinterpret_cast<u2 *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) = packed;
 }
 
 // ------------------------------------------------------------------- K_proj
@@ -418,7 +431,7 @@ hipError_t launch_proj_t(const DevState &st, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_rec(const DevState &st, hipStream_t s) {
-  const int G = ((st.d + BV - 1) / BV) * ((st.R_max + BR - 1) / BR);
+  const int G = (st.d / RT) * ((st.R_max + RT - 1) / RT);
   if (st.dtype == 1)
     hipLaunchKernelGGL(k_rec_bf16, dim3(G), dim3(THREADS), 0, s, st);
   else
