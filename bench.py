@@ -105,6 +105,7 @@ def main():
     proj_ms, proj_launches = dec.timing()
     dec.set_timing(False)
     st = dec.stats()            # counters of the last run
+    hist, hist_w = dec.rows_histogram()
     t1 = time.perf_counter()
     hyps = dec.collect()
     collect_s = time.perf_counter() - t1
@@ -130,6 +131,8 @@ def main():
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": None, "launches": proj_launches,
                      "avg_launch_us": proj_ms * 1e3 / max(proj_launches, 1)},
+        "rows_per_step_hist": {"bucket_width": hist_w,
+                               "counts": {str(i * hist_w): c for i, c in enumerate(hist) if c}},
         "projection_share_of_step": (proj_ms * 1e-3) / elapsed if elapsed > 0 else None,
         "collect_d2h_ms": collect_s * 1e3,
         "pcie_inclusive_hyps_per_s": st["hyps"] / (per_run + collect_s),

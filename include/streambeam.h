@@ -158,6 +158,11 @@ sb_status sb_collect(sb_decoder *dec, sb_hyp *hyps, int64_t hyp_cap, int32_t *to
 /* Counters since create/reset. Synchronizes the stream. */
 sb_status sb_stats(sb_decoder *dec, sb_stats_t *out);
 
+/* Timesteps by number of rows (active candidates) expanded: counts[b] is the
+ * number of timesteps with b*w <= rows < (b+1)*w, w = *bucket_width (the last
+ * bucket also takes everything above). counts: host [64]. Synchronizes. */
+sb_status sb_rows_histogram(sb_decoder *dec, int64_t *counts, int32_t *bucket_width);
+
 /* Forget all inputs, beams, outputs and counters (the queue restarts at
  * position 0). Asynchronous on the stream. */
 sb_status sb_reset(sb_decoder *dec);

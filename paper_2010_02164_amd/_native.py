@@ -80,6 +80,7 @@ def lib():
         "sb_collect": (c_int32, [c_void_p, P(SbHyp), c_int64, P(c_int32), c_int64, P(c_int64), P(c_int64)]),
         "sb_stats": (c_int32, [c_void_p, P(SbStats)]),
         "sb_reset": (c_int32, [c_void_p]),
+        "sb_rows_histogram": (c_int32, [c_void_p, P(c_int64), P(c_int32)]),
         "sb_set_timing": (c_int32, [c_void_p, c_int32]),
         "sb_timing": (c_int32, [c_void_p, P(c_double), P(c_int64)]),
         "sb_debug_expand": (c_int32, [c_void_p, c_int32, c_void_p, P(c_int32), P(c_int32), P(c_int32),

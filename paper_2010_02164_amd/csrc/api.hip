@@ -41,7 +41,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, s_status, s_score, s_tok, s_h,
       s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, total;
+      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -89,6 +89,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.o_count = take(Q * 4);
   L.o_hyp = take(Q * k * sizeof(OutHyp));
   L.o_tok = take(Q * k * MLC * 4);
+  L.wout_t = take(S * 128 * d * es);
   if (m.kv_layers > 0) {
     const size_t planes = (size_t)m.kv_layers * 2;
     L.kv0 = take(nk * planes * MLC * d * 2);
@@ -119,6 +120,9 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   if (p->sched < SB_FIXED || p->sched > SB_VAR_STREAM) return bad(SB_E_INVALID_ARG, "unknown scheduler");
   if (p->max_len_cap < 1 || p->max_len_cap > 4096) return bad(SB_E_INVALID_ARG, "max_len_cap must be in [1, 4096]");
   if (p->max_inputs < 1) return bad(SB_E_INVALID_ARG, "max_inputs must be >= 1");
+  const int64_t es = m->dtype == SB_BF16 ? 2 : 4;
+  if ((int64_t)(m->vocab + 127) / 128 * 128 * m->d * es >= (1ll << 32) || (int64_t)p->n * p->k * m->d * es >= (1ll << 32))
+    return bad(SB_E_UNSUPPORTED, "W_out and the row-state buffer must each be under 4 GiB");
   if (m->kv_layers < 0 || m->kv_layers > 8) return bad(SB_E_UNSUPPORTED, "kv_layers must be in [0, 8]");
   if (m->kv_layers > 0 && m->dtype != SB_BF16) return bad(SB_E_UNSUPPORTED, "KV state requires bf16");
   if (m->kv_layers > 0 && !m->W_kv) return bad(SB_E_INVALID_ARG, "W_kv is NULL");
@@ -270,6 +274,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.W_h = model->W_h;
   st.E = model->E;
   st.W_out = model->W_out;
+  st.wout_t = w + L.wout_t;
   const sb_params &p = dec->params;
   st.n = p.n;
   st.k = p.k;
@@ -284,6 +289,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.kv_layers = model->kv_layers;
   st.max_inputs = p.max_inputs;
   st.kbucket = kbucket_of(p.k);
+  st.hist_width = std::max(16, (st.R_max + 63) / 64);
   st.delta = p.delta;
   st.beta = model->eos_beta;
 
@@ -300,6 +306,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   for (int i = 0; i < 2; ++i)
     if (hipEventCreateWithFlags(&dec->poll_ev[i], hipEventDisableTiming) != hipSuccess) return fail(SB_E_HIP);
   if (launch_init(st, dec->stream) != hipSuccess) return fail(SB_E_HIP);
+  if (launch_relayout_wout(st, dec->stream) != hipSuccess) return fail(SB_E_HIP);
   if (model->kv_layers > 0 &&
       launch_transpose_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
     return fail(SB_E_HIP);
@@ -480,6 +487,16 @@ sb_status sb_stats(sb_decoder *dec, sb_stats_t *out) {
   out->admitted = c.admitted;
   out->hyps = c.hyps;
   out->finished = c.finished;
+  return SB_OK;
+}
+
+sb_status sb_rows_histogram(sb_decoder *dec, int64_t *counts, int32_t *bucket_width) {
+  if (!dec || !counts || !bucket_width) return SB_E_INVALID_ARG;
+  DevCtrl c;
+  HIPCHK(hipMemcpyAsync(&c, dec->st.ctrl, sizeof(DevCtrl), hipMemcpyDeviceToHost, dec->stream));
+  HIPCHK(hipStreamSynchronize(dec->stream));
+  for (int i = 0; i < 64; ++i) counts[i] = c.rows_hist[i];
+  *bucket_width = dec->st.hist_width;
   return SB_OK;
 }
 

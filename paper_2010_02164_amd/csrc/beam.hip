@@ -37,11 +37,7 @@ __global__ __launch_bounds__(256) void k_rowmerge(DevState st) {
   for (int t = lane; t < st.S; t += 64) {
     const float *p = base + (size_t)t * PW;
     TopK<KB> o;
-#pragma unroll
-    for (int q = 0; q < KB; ++q) {
-      o.v[q] = p[2 + q];
-      o.i[q] = __float_as_int(p[2 + KB + q]);
-    }
+    topk_load(o, p + 2);
     lse_merge(m, s, p[0], p[1]);
     topk_merge(tk, o);
   }
@@ -59,8 +55,8 @@ __global__ __launch_bounds__(256) void k_rowmerge(DevState st) {
 #pragma unroll
   for (int q = 0; q < KB; ++q) {
     if (lane == q && q < k) {
-      st.top_lp[(size_t)row * k + q] = (double)tk.v[q] - lse;
-      st.top_tok[(size_t)row * k + q] = tk.i[q];
+      st.top_lp[(size_t)row * k + q] = (double)key_val(tk.k[q]) - lse;
+      st.top_tok[(size_t)row * k + q] = key_idx(tk.k[q]);
     }
   }
 }
@@ -222,24 +218,29 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     st.b_steps[b] = t;
     st.b_par[b] ^= 1;
   }
-  // State copy: s_h[rank] <- hbuf[row(parent)] for every active survivor.
-  // All survivors' loads are issued before any store (up to k rows in flight).
+  // State copy: s_h[rank] <- hbuf[row(parent)] for every active survivor,
+  // flattened over (survivor, 16-byte chunk) so all threads stream.
   const int rowbytes = st.d * (st.dtype == 1 ? 2 : 4);
   const int chunks = rowbytes / 16;
-  int prow[KMAX_SUPPORTED];
-#pragma unroll
-  for (int r = 0; r < KMAX_SUPPORTED; ++r)
-    prow[r] = (r < w && nstat[r] == SLOT_ACTIVE) ? st.s_row[base + npar[r]] : -1;
-  const unsigned char *hb = static_cast<const unsigned char *>(st.hbuf);
-  unsigned char *sh = static_cast<unsigned char *>(st.s_h);
-  for (int c = lane; c < chunks; c += BEAM_THREADS) {
-    uint4 v[KMAX_SUPPORTED];
-#pragma unroll
-    for (int r = 0; r < KMAX_SUPPORTED; ++r)
-      if (prow[r] >= 0) v[r] = reinterpret_cast<const uint4 *>(hb + (size_t)prow[r] * rowbytes)[c];
-#pragma unroll
-    for (int r = 0; r < KMAX_SUPPORTED; ++r)
-      if (prow[r] >= 0) reinterpret_cast<uint4 *>(sh + (size_t)(base + r) * rowbytes)[c] = v[r];
+  __shared__ int cp_src[KMAX_SUPPORTED], cp_dst[KMAX_SUPPORTED];
+  __shared__ int ncopy;
+  if (lane == 0) {
+    int c = 0;
+    for (int r = 0; r < w; ++r)
+      if (nstat[r] == SLOT_ACTIVE) {
+        cp_src[c] = st.s_row[base + npar[r]];
+        cp_dst[c] = base + r;
+        ++c;
+      }
+    ncopy = c;
+  }
+  __syncthreads();
+  const uint4 *__restrict__ hb = static_cast<const uint4 *>(st.hbuf);
+  uint4 *__restrict__ sh = static_cast<uint4 *>(st.s_h);
+  const int total = ncopy * chunks;
+  for (int x = lane; x < total; x += BEAM_THREADS) {
+    const int r = x / chunks, c = x - r * chunks;
+    sh[(size_t)cp_dst[r] * chunks + c] = hb[(size_t)cp_src[r] * chunks + c];
   }
 }
 

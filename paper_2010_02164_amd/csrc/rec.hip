@@ -1,0 +1,187 @@
+// Recurrence of the synthetic decoder D (Sec. 2) on gfx950 MFMA:
+//   h = tanh(W_h h_prev + E[y])      [R,d] x [d,d]^T, fused epilogue
+// W_h (out-feature rows) is the MFMA A operand and the previous states the B
+// operand, both K-contiguous. bf16 workloads accumulate in fp64 (see k_rec_bf16).
+#include "mfma_common.h"
+
+namespace sb {
+namespace {
+
+constexpr int THREADS = 256;
+
+// Round a binary64 value to bfloat16 (nearest, ties to even) directly, with
+// no float intermediate: keep 8 significant bits; below bf16's smallest
+// normal (2^-126) the step is the subnormal quantum 2^-133.
+__device__ __forceinline__ uint16_t bf16_rne_from_double(double x) {
+  const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+  const unsigned long long sign = u & 0x8000000000000000ull;
+  unsigned long long a = u & 0x7FFFFFFFFFFFFFFFull;
+  const int e = (int)(a >> 52);
+  float f;
+  if (e >= 1023 - 126) {
+    const unsigned long long lsb = (a >> 45) & 1ull;
+    a += 0x0FFFFFFFFFFFull + lsb;   // half of the dropped 45 bits, minus one
+    a &= ~0x1FFFFFFFFFFFull;
+    f = (float)__longlong_as_double((long long)(a | sign));
+  } else {
+    const double q = 0x1p-133;
+    f = (float)(rint(x / q) * q);
+  }
+  return (uint16_t)(__float_as_uint(f) >> 16);
+}
+
+// ---------------------------------------------------------------- K_rec
+// The recurrence GEMM is small ([R,d] x [d,d]) next to the projection, so it
+// is cut into 32 (out features) x 32 (rows) tiles to reach hundreds of
+// workgroups, and the K loop of each tile is split over the 4 waves of the
+// workgroup; the 4 partial sums are added in a fixed order (wave 0 + 1 + 2
+// + 3), so the result does not depend on which rows share the step. Operands
+// are read straight from global memory (W_h and the states are L2/MALL
+// resident); each lane loads the 16 bytes it feeds to the MFMA.
+constexpr int RT = 32;        // tile edge
+constexpr int RSPLIT = 4;     // K split over the waves
+
+__device__ __forceinline__ const unsigned char *rec_state_row(const DevState &st, int r, int R, int rowbytes) {
+  return state_row(st, min(r, R - 1), rowbytes);
+}
+
+__global__ __launch_bounds__(THREADS) void k_rec_f32(DevState st) {
+  const int R = st.ctrl->R;
+  const int d = st.d;
+  const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
+  int vt, rt;
+  if (!tile_of(nvt, nrt, vt, rt)) return;
+  const int v0 = vt * RT, r0 = rt * RT;
+  if (r0 >= R) return;
+  __shared__ float red[RSPLIT][RT * RT];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rowbytes = d * 4;
+  const int kq = d / RSPLIT;                       // K range of this wave
+  const float *arow = static_cast<const float *>(st.W_h) + (size_t)(v0 + (lane & 31)) * d + w * kq;
+  const float *brow = reinterpret_cast<const float *>(rec_state_row(st, r0 + (lane & 31), R, rowbytes)) + w * kq;
+  const int h = (lane >> 5) * 4;
+  f16v acc = {};
+#pragma unroll 4
+  for (int kk = 0; kk < kq; kk += 8) {
+    const f4 a = *reinterpret_cast<const f4 *>(arow + kk + h);
+    const f4 b = *reinterpret_cast<const f4 *>(brow + kk + h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc, 0, 0, 0);
+  }
+  // acc: out feature i = 8*(reg/4) + 4*(lane/32) + reg%4, row j = lane%32.
+#pragma unroll
+  for (int reg = 0; reg < 16; ++reg) {
+    const int i = 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
+    red[w][(lane & 31) * RT + i] = acc[reg];
+  }
+  __syncthreads();
+  // 256 threads x 4 outputs: thread -> row j = tid/8, features 4*(tid%8)..+3.
+  const int j = threadIdx.x >> 3, i0 = (threadIdx.x & 7) * 4;
+  const int row = r0 + j;
+  if (row >= R) return;
+  const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+  const f4 e = *reinterpret_cast<const f4 *>(E);
+  f4 hv;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int o = j * RT + i0 + q;
+    const float pre = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
+    hv[q] = tanhf(pre + e[q]);
+  }
+  *reinterpret_cast<f4 *>(static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0) = hv;
+}
+
+// bf16 states are rounded after tanh, a discontinuous map: any difference
+// in the pre-activation can flip a rounding and then grows step after step.
+// Products of two bf16 values are exact in fp64 and so is their sum over
+// the state size in practice, so the pre-activation is accumulated with the
+// fp64 MFMA (16x16x4), tanh taken in fp64 and the result rounded once.
+__global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
+  const int R = st.ctrl->R;
+  const int d = st.d;
+  const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
+  int vt, rt;
+  if (!tile_of(nvt, nrt, vt, rt)) return;
+  const int v0 = vt * RT, r0 = rt * RT;
+  if (r0 >= R) return;
+  __shared__ double red[RSPLIT][RT * RT];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rowbytes = d * 2;
+  const int kq = d / RSPLIT;
+  const int r16 = lane & 15, g = lane >> 4;
+  // A: 2 blocks of 16 out features, B: 2 blocks of 16 rows; the lane feeds
+  // 4 consecutive bf16 at k = kk + 4g to 4 MFMAs (same permutation for A, B).
+  const uint16_t *a0 = static_cast<const uint16_t *>(st.W_h) + (size_t)(v0 + r16) * d + w * kq + 4 * g;
+  const uint16_t *a1 = a0 + (size_t)16 * d;
+  const uint16_t *b0 = reinterpret_cast<const uint16_t *>(rec_state_row(st, r0 + r16, R, rowbytes)) + w * kq + 4 * g;
+  const uint16_t *b1 = reinterpret_cast<const uint16_t *>(rec_state_row(st, r0 + 16 + r16, R, rowbytes)) + w * kq + 4 * g;
+  d4 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+  auto cvt = [](u2 raw, double *o) {
+    o[0] = (double)__uint_as_float(raw[0] << 16);
+    o[1] = (double)__uint_as_float(raw[0] & 0xFFFF0000u);
+    o[2] = (double)__uint_as_float(raw[1] << 16);
+    o[3] = (double)__uint_as_float(raw[1] & 0xFFFF0000u);
+  };
+#pragma unroll 2
+  for (int kk = 0; kk < kq; kk += 16) {
+    double a[2][4], b[2][4];
+    cvt(*reinterpret_cast<const u2 *>(a0 + kk), a[0]);
+    cvt(*reinterpret_cast<const u2 *>(a1 + kk), a[1]);
+    cvt(*reinterpret_cast<const u2 *>(b0 + kk), b[0]);
+    cvt(*reinterpret_cast<const u2 *>(b1 + kk), b[1]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x][e], b[y][e], acc[x][y], 0, 0, 0);
+  }
+  // f64 16x16x4 result: lane l, register q hold out feature (l/16) + 4q of
+  // the block and row l%16.
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = x * 16 + g + 4 * q, j = y * 16 + r16;
+        red[w][j * RT + i] = acc[x][y][q];
+      }
+  __syncthreads();
+  const int j = threadIdx.x >> 3, i0 = (threadIdx.x & 7) * 4;
+  const int row = r0 + j;
+  if (row >= R) return;
+  const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+  const u2 eraw = *reinterpret_cast<const u2 *>(E);
+  double e[4];
+  cvt(eraw, e);
+  uint16_t hb[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int o = j * RT + i0 + q;
+    const double pre = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
+    hb[q] = bf16_rne_from_double(tanh(pre + e[q]));
+  }
+  u2 packed;
+  packed[0] = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+  packed[1] = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
+  *reinterpret_cast<u2 *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) = packed;
+}
+
+}  // namespace
+
+hipError_t launch_rec(const DevState &st, hipStream_t s) {
+  const int G = xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT));
+  if (st.dtype == 1)
+    hipLaunchKernelGGL(k_rec_bf16, dim3(G), dim3(THREADS), 0, s, st);
+  else
+    hipLaunchKernelGGL(k_rec_f32, dim3(G), dim3(THREADS), 0, s, st);
+  return hipGetLastError();
+}
+
+}  // namespace sb

@@ -25,6 +25,7 @@ struct DevCtrl {
   int32_t n_sel;      // beams selected this step
   int32_t pad0;
   int64_t timesteps, expansions, noops, refills, admitted, hyps, finished;
+  int64_t rows_hist[64];   // timesteps by rows expanded, bucket = R / hist_width
 };
 
 // A finalized hypothesis. The beam kernel records where its history ends
@@ -75,9 +76,14 @@ struct DevState {
   uint16_t *wkvT;      // [L*2*d][d]  (transposed W_kv: out-feature major)
   // model
   const void *W_h, *E, *W_out;
+  // W_out re-laid out tile-contiguous: [S][nk][128 rows][128 bytes], one
+  // 16 KB block per (128-row vocabulary tile, 128-byte K chunk); rows >= V
+  // are zero.
+  unsigned char *wout_t;
   // sizes and parameters
   int32_t n, k, d, V, M, max_len_cap, refill_thr, S, R_max, dtype, kv_layers, max_inputs;
   int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
+  int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   double delta;
   float beta;
 };
@@ -98,6 +104,7 @@ hipError_t launch_kv_append(const DevState &st, hipStream_t s);
 hipError_t launch_kv_gather(const DevState &st, hipStream_t s);
 hipError_t launch_backtrack(const DevState &st, int q0, int q1, hipStream_t s);
 hipError_t launch_init(const DevState &st, hipStream_t s);
+hipError_t launch_relayout_wout(const DevState &st, hipStream_t s);
 hipError_t launch_transpose_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s);
 
 }  // namespace sb

@@ -151,6 +151,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     c->t_sel = R > 0 ? mn + 1 : 0;
     c->done = R == 0 ? 1 : 0;
     if (R > 0) {
+      c->rows_hist[min(63, R / st.hist_width)] += 1;
       c->timesteps += 1;
       c->expansions += R;
       c->noops += noops;

@@ -1,6 +1,11 @@
 // Register-resident top-K lists and log-sum-exp pairs for the projection
-// epilogue and the row merge. Order: larger value first; equal values are
-// ordered by smaller token id (the ranking key of the search).
+// epilogue and the row merge.
+//
+// A candidate (logit value v, token id i) is packed into one 64-bit key that
+// orders exactly like the search's ranking key: larger value first, equal
+// values by smaller token id. High word: the float's bits mapped to an
+// order-preserving unsigned integer; low word: ~i. Key 0 is "empty" and
+// ranks below every real candidate (even a -inf logit).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -9,92 +14,100 @@
 
 namespace sb {
 
-constexpr int TOPK_NONE = 0x7fffffff;
+typedef unsigned long long cand_key;
+
+__device__ __forceinline__ cand_key make_key(float v, int idx) {
+  uint32_t u = __float_as_uint(v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((cand_key)u << 32) | (uint32_t)(~idx);
+}
+__device__ __forceinline__ float key_val(cand_key k) {
+  uint32_t u = (uint32_t)(k >> 32);
+  u = (u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u;
+  return __uint_as_float(u);
+}
+__device__ __forceinline__ int key_idx(cand_key k) { return (int)(~(uint32_t)k); }
 
 template <int K>
 struct TopK {
-  float v[K];
-  int i[K];
+  cand_key k[K];   // sorted, best first
 };
-
-__device__ __forceinline__ bool key_beats(float va, int ia, float vb, int ib) {
-  return va > vb || (va == vb && ia < ib);
-}
 
 template <int K>
 __device__ __forceinline__ void topk_init(TopK<K> &t) {
 #pragma unroll
-  for (int j = 0; j < K; ++j) {
-    t.v[j] = -INFINITY;
-    t.i[j] = TOPK_NONE;
-  }
+  for (int j = 0; j < K; ++j) t.k[j] = 0ull;
 }
 
-// Insert a value whose id is larger than every id already inserted (ids are
-// pushed in increasing order), so strict '>' keeps equal values in id order.
-template <int K>
-__device__ __forceinline__ void topk_push_ordered(TopK<K> &t, float v, int id) {
-  if (v > t.v[K - 1]) {
+// Compare-exchange: after it, a holds the larger key when `desc`.
+__device__ __forceinline__ void cex(cand_key &a, cand_key &b, bool desc) {
+  const bool sw = desc ? (b > a) : (a > b);
+  const cand_key x = sw ? b : a, y = sw ? a : b;
+  a = x;
+  b = y;
+}
+
+// Sort N keys (N a power of two) best first with a bitonic network.
+template <int N>
+__device__ __forceinline__ void bitonic_sort_desc(cand_key *a) {
 #pragma unroll
-    for (int j = K - 1; j > 0; --j) {
-      const bool up = v > t.v[j - 1];
-      const bool here = v > t.v[j];
-      const float nv = up ? t.v[j - 1] : (here ? v : t.v[j]);
-      const int ni = up ? t.i[j - 1] : (here ? id : t.i[j]);
-      t.v[j] = nv;
-      t.i[j] = ni;
-    }
-    if (v > t.v[0]) {
-      t.v[0] = v;
-      t.i[0] = id;
-    }
-  }
+  for (int k = 2; k <= N; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) cex(a[i], a[l], (i & k) == 0);
+      }
 }
 
-// a <- best K of (a union b); both sorted. Bitonic: pairing a[j] with
-// b[K-1-j] keeps the K best in a bitonic sequence, half-cleaners sort it.
+// a <- best K of (a union b); both sorted best first. Pairing a[j] with
+// b[K-1-j] keeps the K best as a bitonic sequence; half-cleaners sort it.
 template <int K>
 __device__ __forceinline__ void topk_merge(TopK<K> &a, const TopK<K> &b) {
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    const float bv = b.v[K - 1 - j];
-    const int bi = b.i[K - 1 - j];
-    if (!key_beats(a.v[j], a.i[j], bv, bi)) {
-      a.v[j] = bv;
-      a.i[j] = bi;
-    }
+    const cand_key o = b.k[K - 1 - j];
+    a.k[j] = a.k[j] > o ? a.k[j] : o;
   }
 #pragma unroll
-  for (int s = K / 2; s > 0; s >>= 1) {
+  for (int s = K / 2; s > 0; s >>= 1)
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-      if ((j & s) == 0) {
-        const float v0 = a.v[j], v1 = a.v[j + s];
-        const int i0 = a.i[j], i1 = a.i[j + s];
-        const bool sw = key_beats(v1, i1, v0, i0);
-        a.v[j] = sw ? v1 : v0;
-        a.i[j] = sw ? i1 : i0;
-        a.v[j + s] = sw ? v0 : v1;
-        a.i[j + s] = sw ? i0 : i1;
-      }
-    }
-  }
+    for (int j = 0; j < K; ++j)
+      if ((j & s) == 0) cex(a.k[j], a.k[j + s], true);
 }
 
 template <int K>
 __device__ __forceinline__ void topk_shfl_xor(TopK<K> &out, const TopK<K> &in, int mask) {
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    out.v[j] = __shfl_xor(in.v[j], mask, 64);
-    out.i[j] = __shfl_xor(in.i[j], mask, 64);
+    const uint32_t lo = __shfl_xor((uint32_t)in.k[j], mask, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(in.k[j] >> 32), mask, 64);
+    out.k[j] = ((cand_key)hi << 32) | lo;
   }
+}
+
+// Stored as two 32-bit words (low, high) in a float array.
+template <int K>
+__device__ __forceinline__ void topk_store(float *p, const TopK<K> &t) {
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    p[2 * j] = __uint_as_float((uint32_t)t.k[j]);
+    p[2 * j + 1] = __uint_as_float((uint32_t)(t.k[j] >> 32));
+  }
+}
+template <int K>
+__device__ __forceinline__ void topk_load(TopK<K> &t, const float *p) {
+#pragma unroll
+  for (int j = 0; j < K; ++j)
+    t.k[j] = ((cand_key)__float_as_uint(p[2 * j + 1]) << 32) | __float_as_uint(p[2 * j]);
 }
 
 // (m, s) represents log(s) + m: a running max and a sum of exp(z - m).
 __device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2) {
   const float M = fmaxf(m, m2);
   if (M == -INFINITY) return;
-  s = s * expf(m - M) + s2 * expf(m2 - M);
+  s = s * __expf(m - M) + s2 * __expf(m2 - M);
   m = M;
 }
 

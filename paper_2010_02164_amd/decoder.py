@@ -167,6 +167,14 @@ class Decoder:
         _check(N.lib().sb_stats(self.handle, ctypes.byref(s)), "sb_stats", self.handle)
         return {f: int(getattr(s, f)) for f, _ in N.SbStats._fields_}
 
+    def rows_histogram(self):
+        """(counts[64], bucket width): timesteps by rows expanded."""
+        counts = (ctypes.c_int64 * 64)()
+        w = ctypes.c_int32(0)
+        _check(N.lib().sb_rows_histogram(self.handle, counts, ctypes.byref(w)), "sb_rows_histogram",
+               self.handle)
+        return [int(c) for c in counts], int(w.value)
+
     # -- timing ---------------------------------------------------------------
     def set_timing(self, enable: bool):
         _check(N.lib().sb_set_timing(self.handle, int(enable)), "sb_set_timing", self.handle)
