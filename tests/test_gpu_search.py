@@ -50,3 +50,25 @@ def test_deterministic(gpu):
     assert sa == sb
     for ya, yb in zip(a, b):
         assert [(h.tokens, h.score) for h in ya] == [(h.tokens, h.score) for h in yb]
+
+
+def test_cfg3_full_size_sampled(gpu):
+    # The full MT-shaped fp32 workload (4096 inputs, |V| = 32000) in the
+    # configuration the benchmark runs; a sample of inputs is decoded by the
+    # oracle one at a time (results are per input, Sec. 3).
+    from oracle.compare import compare
+    from oracle.search import decode_workload
+    from synthgen import get_config
+    wl = make_workload(get_config(3))
+    g, st, dec = gpu_decode(wl, "var_stream")
+    dec.close()
+    assert st["finished"] == len(wl.Lx) and st["hyps"] == sum(len(y) for y in g)
+    sample = [0, 1, 777, 2048, 4095]
+    hy, mm = [], []
+    for i in sample:
+        o = decode_workload(wl, inputs=[i])
+        hy.append(o.hyps[0])
+        mm.append(o.min_margin[0])
+    rep = compare(hy, mm, [[(h.tokens, h.score, h.status) for h in g[i]] for i in sample], inputs=sample)
+    print(f"[parity] cfg3 full, sampled: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures
