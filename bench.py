@@ -4,7 +4,10 @@ A bench "step" is one whole decode of the workload: queue every input
 (device-resident encodings), run the search until every beam is finished
 (refill, selection, expansion, top-k, pruning, finalization, state reorder,
 and the rebuild of the output tokens, all in device memory). Output copies
-to the host are outside the timed region and reported separately.
+to the host are outside the timed region and reported separately. The
+timed region runs with projection timing on (kernels launched one by one,
+HIP events around each projection launch); the same decodes replayed as
+captured step graphs are reported as graph_replay_hyps_per_s.
 
 Default workload: the MT-shaped fp32 configuration (N=4096 inputs, n=128,
 k=5, |V|=32000, d=1024, Var-Stream eps=1/4, delta=1.5), synthetic.
@@ -111,6 +114,14 @@ def main():
     collect_s = time.perf_counter() - t1
     assert len(hyps) == st["hyps"]
 
+    # The same workload replayed as captured step graphs, untimed kernels.
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        run_once()
+    torch.cuda.synchronize()
+    graph_per_run = (time.perf_counter() - t2) / args.steps
+
     per_run = elapsed / args.steps
     hyps_per_s = st["hyps"] / per_run
     exps_per_s = st["expansions"] / per_run
@@ -134,6 +145,7 @@ def main():
         "rows_per_step_hist": {"bucket_width": hist_w,
                                "counts": {str(i * hist_w): c for i, c in enumerate(hist) if c}},
         "projection_share_of_step": (proj_ms * 1e-3) / elapsed if elapsed > 0 else None,
+        "graph_replay_hyps_per_s": st["hyps"] / graph_per_run,
         "collect_d2h_ms": collect_s * 1e3,
         "pcie_inclusive_hyps_per_s": st["hyps"] / (per_run + collect_s),
     }

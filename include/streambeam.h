@@ -85,7 +85,8 @@ typedef struct {
  *         the rows bf16(h . W_kv[l][j]) to the candidate's KV-like state. */
 typedef struct {
   int32_t vocab;         /* |V| >= 2                                               */
-  int32_t d;             /* state size, multiple of 32, 32..4096                  */
+  int32_t d;             /* state size in [64, 4096], a multiple of 64 (fp32) or
+                            of 128 (bf16)                                        */
   int32_t dtype;         /* sb_dtype                                               */
   float   eos_beta;      /* EOS bias slope beta                                    */
   const void *W_h, *E, *W_out;
@@ -143,7 +144,9 @@ sb_status sb_step(sb_decoder *dec, int32_t *done);
 
 /* Step until every submitted input is finished, then rebuild the tokens of
  * every finished hypothesis in device memory; returns after the stream has
- * completed the work. */
+ * completed the work. Steps run as a captured HIP graph of 8 timesteps,
+ * replayed on the decoder's stream (captured on first use; the library keeps
+ * a private capture stream). Timesteps past completion are no-ops. */
 sb_status sb_run(sb_decoder *dec);
 
 /* Copy finalized hypotheses to the host, in input order then rank order,
@@ -167,8 +170,10 @@ sb_status sb_rows_histogram(sb_decoder *dec, int64_t *counts, int32_t *bucket_wi
  * position 0). Asynchronous on the stream. */
 sb_status sb_reset(sb_decoder *dec);
 
-/* Enable (1) or disable (0) per-kernel timing with HIP events on the
- * decoder's stream around the vocabulary-projection kernel of every step. */
+/* Enable (1) or disable (0) timing of the vocabulary-projection kernel:
+ * sb_run then launches the step kernels one by one (instead of replaying the
+ * step graph) and brackets every projection launch with a pair of HIP events
+ * recorded on the decoder's stream. */
 sb_status sb_set_timing(sb_decoder *dec, int32_t enable);
 
 /* Sum of the timed projection-kernel durations (ms) and the number of timed

@@ -27,10 +27,16 @@ struct sb_decoder {
   int32_t *pinned_flag = nullptr;  // [2] done-flag readback
   hipEvent_t poll_ev[2] = {nullptr, nullptr};
   bool timing = false;
-  std::vector<hipEvent_t> tev;  // pairs around the projection kernel
-  int tev_used = 0;
   double proj_ms = 0.0;
   int64_t proj_launches = 0;
+  // A burst of timesteps captured once as a HIP graph (untimed runs).
+  hipStream_t cap_stream = nullptr;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t graph_exec = nullptr;
+  // Timed runs launch kernel by kernel with an event pair around every
+  // projection launch, taken from this pool.
+  std::vector<hipEvent_t> tev;
+  int tev_used = 0;
   std::string err;
 };
 
@@ -108,11 +114,11 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   };
   if (!m || !p) return bad(SB_E_INVALID_ARG, "null model or params");
   if (m->dtype != SB_F32 && m->dtype != SB_BF16) return bad(SB_E_INVALID_ARG, "unknown dtype");
-  if (m->d < 32 || m->d > 4096 || m->d % 32) return bad(SB_E_UNSUPPORTED, "d must be a multiple of 32 in [32, 4096]");
-  if (m->dtype == SB_BF16 && m->d % 64) return bad(SB_E_UNSUPPORTED, "bf16 needs d a multiple of 64");
+  if (m->d < 64 || m->d > 4096 || m->d % 64) return bad(SB_E_UNSUPPORTED, "d must be a multiple of 64 in [64, 4096]");
+  if (m->dtype == SB_BF16 && m->d % 128) return bad(SB_E_UNSUPPORTED, "bf16 needs d a multiple of 128");
   if (p->k < 1 || p->k > KMAX_SUPPORTED) return bad(SB_E_UNSUPPORTED, "k must be in [1, 16]");
   if (m->vocab < 2 || m->vocab < p->k || m->vocab > (1 << 23)) return bad(SB_E_INVALID_ARG, "vocab must be in [max(2,k), 2^23]");
-  if (!(p->n >= 1 && p->n <= 4096)) return bad(SB_E_UNSUPPORTED, "n must be in [1, 4096]");
+  if (!(p->n >= 1 && p->n <= 4096)) return bad(SB_E_UNSUPPORTED, "n must be in [1, 4096]");  // 4 beams per scheduler thread
   if ((int64_t)p->n * p->k > 65536) return bad(SB_E_UNSUPPORTED, "n*k must be <= 65536");
   if (!(p->eps >= 0.0 && p->eps < 1.0)) return bad(SB_E_INVALID_ARG, "eps must be in [0, 1)");
   if (!(p->delta > 0.0)) return bad(SB_E_INVALID_ARG, "delta must be > 0 (use +inf to disable)");
@@ -158,36 +164,65 @@ __global__ void k_set_queued(DevCtrl *c, int32_t nq) {
 
 __global__ void k_set_rows(DevCtrl *c, int32_t R) { c->R = R; }
 
-sb_status launch_step(sb_decoder *dec) {
+constexpr int BURST = 8;   // timesteps per graph launch / per done-flag poll
+
+// One timestep of Alg. 1. With e0/e1 given, HIP events bracket the
+// projection kernel.
+sb_status launch_step(sb_decoder *dec, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
   const DevState &st = dec->st;
-  hipStream_t s = dec->stream;
   HIPCHK(launch_sched(st, s));
   HIPCHK(launch_rec(st, s));
   if (st.kv_layers > 0) HIPCHK(launch_kv_append(st, s));
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (dec->timing) {
-    if (dec->tev_used + 2 > (int)dec->tev.size()) {
-      // harvest the pool
-      HIPCHK(hipStreamSynchronize(s));
-      for (int i = 0; i + 1 < dec->tev_used; i += 2) {
-        float ms = 0.f;
-        HIPCHK(hipEventElapsedTime(&ms, dec->tev[i], dec->tev[i + 1]));
-        dec->proj_ms += ms;
-        dec->proj_launches += 1;
-      }
-      dec->tev_used = 0;
-    }
-    e0 = dec->tev[dec->tev_used];
-    e1 = dec->tev[dec->tev_used + 1];
-    dec->tev_used += 2;
-    HIPCHK(hipEventRecord(e0, s));
-  }
+  if (e0) HIPCHK(hipEventRecord(e0, s));
   HIPCHK(launch_proj(st, s));
-  if (dec->timing) HIPCHK(hipEventRecord(e1, s));
+  if (e1) HIPCHK(hipEventRecord(e1, s));
   HIPCHK(launch_rowmerge(st, s));
   HIPCHK(launch_beam(st, s));
   if (st.kv_layers > 0) HIPCHK(launch_kv_gather(st, s));
   return SB_OK;
+}
+
+// Capture BURST timesteps as a graph on a private stream (the caller's
+// stream may be the legacy default stream, which cannot be captured).
+sb_status capture(sb_decoder *dec, hipGraph_t *g_out, hipGraphExec_t *exec_out) {
+  if (!dec->cap_stream) HIPCHK(hipStreamCreateWithFlags(&dec->cap_stream, hipStreamNonBlocking));
+  HIPCHK(hipStreamBeginCapture(dec->cap_stream, hipStreamCaptureModeThreadLocal));
+  sb_status st = SB_OK;
+  for (int i = 0; i < BURST && st == SB_OK; ++i) st = launch_step(dec, dec->cap_stream);
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(dec->cap_stream, &g);
+  if (st != SB_OK) {
+    if (g) (void)hipGraphDestroy(g);
+    return st;
+  }
+  HIPCHK(e);
+  *g_out = g;
+  HIPCHK(hipGraphInstantiate(exec_out, g, nullptr, nullptr, 0));
+  return SB_OK;
+}
+
+// Add the projection times of the used part of the event pool.
+sb_status harvest(sb_decoder *dec) {
+  for (int i = 0; i + 1 < dec->tev_used; i += 2) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, dec->tev[i], dec->tev[i + 1]));
+    dec->proj_ms += ms;
+    dec->proj_launches += 1;
+  }
+  dec->tev_used = 0;
+  return SB_OK;
+}
+
+// One timed timestep: events from the pool bracket the projection.
+sb_status launch_timed_step(sb_decoder *dec) {
+  if (dec->tev_used + 2 > (int)dec->tev.size()) {
+    HIPCHK(hipStreamSynchronize(dec->stream));
+    sb_status s = harvest(dec);
+    if (s != SB_OK) return s;
+  }
+  hipEvent_t e0 = dec->tev[dec->tev_used], e1 = dec->tev[dec->tev_used + 1];
+  dec->tev_used += 2;
+  return launch_step(dec, dec->stream, e0, e1);
 }
 
 }  // namespace
@@ -362,7 +397,7 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_
 
 sb_status sb_step(sb_decoder *dec, int32_t *done) {
   if (!dec) return SB_E_INVALID_ARG;
-  sb_status s = launch_step(dec);
+  sb_status s = launch_step(dec, dec->stream);
   if (s != SB_OK) return s;
   if (done) {
     HIPCHK(hipMemcpyAsync(dec->pinned_flag, &dec->st.ctrl->done, sizeof(int32_t), hipMemcpyDeviceToHost,
@@ -378,27 +413,32 @@ sb_status sb_run(sb_decoder *dec) {
   // Every step either expands a live beam or is the final no-op, and a beam
   // takes at most max_len_cap steps, so this bounds any correct run.
   const int64_t limit = ((int64_t)dec->n_queued + dec->params.n) * (dec->params.max_len_cap + 1) + 64;
-  constexpr int BURST = 8;
-  int64_t steps = 0;
-  int slot = 0;
-  bool pending = false;
+  const bool timed = dec->timing;
+  if (!timed && !dec->graph_exec) {
+    sb_status s = capture(dec, &dec->graph, &dec->graph_exec);
+    if (s != SB_OK) return s;
+  }
+  int64_t bursts = 0;
   while (true) {
-    for (int i = 0; i < BURST; ++i) {
-      sb_status s = launch_step(dec);
-      if (s != SB_OK) return s;
+    const int slot = (int)(bursts & 1);
+    if (!timed) {
+      HIPCHK(hipGraphLaunch(dec->graph_exec, dec->stream));
+    } else {
+      for (int i = 0; i < BURST; ++i) {
+        sb_status s = launch_timed_step(dec);
+        if (s != SB_OK) return s;
+      }
     }
-    steps += BURST;
     HIPCHK(hipMemcpyAsync(dec->pinned_flag + slot, &dec->st.ctrl->done, sizeof(int32_t),
                           hipMemcpyDeviceToHost, dec->stream));
     HIPCHK(hipEventRecord(dec->poll_ev[slot], dec->stream));
+    ++bursts;
     // Poll the previous burst's flag while this burst runs.
-    if (pending) {
+    if (bursts >= 2) {
       HIPCHK(hipEventSynchronize(dec->poll_ev[slot ^ 1]));
       if (dec->pinned_flag[slot ^ 1]) break;
     }
-    pending = true;
-    slot ^= 1;
-    if (steps > limit) {
+    if (bursts * BURST > limit) {
       dec->err = "sb_run: step limit exceeded without completion";
       return SB_E_STATE;
     }
@@ -503,7 +543,7 @@ sb_status sb_rows_histogram(sb_decoder *dec, int64_t *counts, int32_t *bucket_wi
 sb_status sb_set_timing(sb_decoder *dec, int32_t enable) {
   if (!dec) return SB_E_INVALID_ARG;
   if (enable && dec->tev.empty()) {
-    dec->tev.resize(2 * 2048, nullptr);
+    dec->tev.resize(2 * 1024, nullptr);
     for (auto &e : dec->tev) HIPCHK(hipEventCreate(&e));
   }
   dec->timing = enable != 0;
@@ -516,13 +556,8 @@ sb_status sb_set_timing(sb_decoder *dec, int32_t enable) {
 sb_status sb_timing(sb_decoder *dec, double *proj_ms, int64_t *proj_launches) {
   if (!dec || !proj_ms || !proj_launches) return SB_E_INVALID_ARG;
   HIPCHK(hipStreamSynchronize(dec->stream));
-  for (int i = 0; i + 1 < dec->tev_used; i += 2) {
-    float ms = 0.f;
-    HIPCHK(hipEventElapsedTime(&ms, dec->tev[i], dec->tev[i + 1]));
-    dec->proj_ms += ms;
-    dec->proj_launches += 1;
-  }
-  dec->tev_used = 0;
+  sb_status s = harvest(dec);
+  if (s != SB_OK) return s;
   *proj_ms = dec->proj_ms;
   *proj_launches = dec->proj_launches;
   return SB_OK;
@@ -616,6 +651,9 @@ sb_status sb_destroy(sb_decoder *dec) {
     if (dec->poll_ev[i]) (void)hipEventDestroy(dec->poll_ev[i]);
   if (dec->pinned_len) (void)hipHostFree(dec->pinned_len);
   if (dec->pinned_flag) (void)hipHostFree(dec->pinned_flag);
+  if (dec->graph_exec) (void)hipGraphExecDestroy(dec->graph_exec);
+  if (dec->graph) (void)hipGraphDestroy(dec->graph);
+  if (dec->cap_stream) (void)hipStreamDestroy(dec->cap_stream);
   delete dec;
   return SB_OK;
 }

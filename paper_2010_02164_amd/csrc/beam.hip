@@ -76,7 +76,8 @@ constexpr int BEAM_THREADS = 256;
 __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const int b = blockIdx.x;
   const int lane = threadIdx.x;   // 0..255
-  if (st.ctrl->R == 0 || !st.b_sel[b]) return;
+  // b_sel is cleared for every beam when nothing is live (R == 0).
+  if (!st.b_sel[b]) return;
   const int k = st.k;
   const int base = b * k;
   __shared__ double cs[MAXC];
@@ -86,34 +87,47 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   __shared__ int npar[KMAX_SUPPORTED], ntok[KMAX_SUPPORTED], nstat[KMAX_SUPPORTED];
   __shared__ int kept_per[KMAX_SUPPORTED];
   __shared__ int nw_sh, nact_sh, nvalid_sh;
+  // The beam's slots, read once (one parallel round of loads).
+  __shared__ int sl_status[KMAX_SUPPORTED], sl_row[KMAX_SUPPORTED];
+  __shared__ double sl_score[KMAX_SUPPORTED];
+  __shared__ int q_in_sh, t_sh, max_len_sh;
 
-  const int q_in = st.b_input[b];
-  const int t = st.b_steps[b] + 1;     // 1-based index of the emitted token
-  const int max_len = st.q_ml[q_in];
+  if (lane < k) {
+    sl_status[lane] = st.s_status[base + lane];
+    sl_row[lane] = st.s_row[base + lane];
+    sl_score[lane] = st.s_score[base + lane];
+  }
+  if (lane == 64) {
+    const int q = st.b_input[b];
+    q_in_sh = q;
+    t_sh = st.b_steps[b] + 1;     // 1-based index of the emitted token
+    max_len_sh = st.q_ml[q];
+  }
+  if (lane == 128) nvalid_sh = 0;
+  if (lane >= 192 && lane < 192 + KMAX_SUPPORTED) at_rank[lane - 192] = -1;
+  __syncthreads();
+  const int q_in = q_in_sh, t = t_sh, max_len = max_len_sh;
 
   // Candidate set: child c of parent j at index j*k + c; no-op of parent j
   // at index k*k + j.
   const int C = k * k + k;
-  if (lane == 0) nvalid_sh = 0;
-  if (lane < KMAX_SUPPORTED) at_rank[lane] = -1;
-  __syncthreads();
   for (int q = lane; q < C; q += BEAM_THREADS) {
     int valid = 0, par, tok = -1;
     double sc = 0.0;
     if (q < k * k) {
       par = q / k;
       const int c = q - par * k;
-      if (st.s_status[base + par] == SLOT_ACTIVE) {
-        const int r = st.s_row[base + par];
-        sc = st.s_score[base + par] + st.top_lp[(size_t)r * k + c];
+      if (sl_status[par] == SLOT_ACTIVE) {
+        const int r = sl_row[par];
+        sc = sl_score[par] + st.top_lp[(size_t)r * k + c];
         tok = st.top_tok[(size_t)r * k + c];
         valid = tok >= 0 && tok < st.V;
       }
     } else {
       par = q - k * k;
-      const int status = st.s_status[base + par];
+      const int status = sl_status[par];
       if (status == SLOT_EOS || status == SLOT_MAXLEN) {
-        sc = st.s_score[base + par];
+        sc = sl_score[par];
         valid = 1;
       }
     }
@@ -149,7 +163,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
       if (sc < ref - st.delta) continue;            // relative threshold
       int status;
       if (tok < 0) {
-        status = st.s_status[base + par];          // no-op keeps EOS / MAXLEN
+        status = sl_status[par];                   // no-op keeps EOS / MAXLEN
       } else {
         if (kept_per[par] >= st.M) continue;       // max candidates per parent
         kept_per[par] += 1;
@@ -208,7 +222,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
       st.s_status[base + lane] = nstat[lane];
       st.s_score[base + lane] = nscore[lane];
       if (ntok[lane] >= 0) st.s_tok[base + lane] = ntok[lane];
-      st.s_prow[base + lane] = nstat[lane] == SLOT_ACTIVE ? st.s_row[base + par] : -1;
+      st.s_prow[base + lane] = nstat[lane] == SLOT_ACTIVE ? sl_row[par] : -1;
     } else {
       st.s_status[base + lane] = SLOT_EMPTY;
       st.s_prow[base + lane] = -1;
@@ -228,7 +242,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     int c = 0;
     for (int r = 0; r < w; ++r)
       if (nstat[r] == SLOT_ACTIVE) {
-        cp_src[c] = st.s_row[base + npar[r]];
+        cp_src[c] = sl_row[npar[r]];
         cp_dst[c] = base + r;
         ++c;
       }

@@ -38,14 +38,15 @@ __device__ __forceinline__ uint16_t bf16_rne_from_double(double x) {
 // + 3), so the result does not depend on which rows share the step. Operands
 // are read straight from global memory (W_h and the states are L2/MALL
 // resident); each lane loads the 16 bytes it feeds to the MFMA.
-constexpr int RT = 32;        // tile edge
-constexpr int RSPLIT = 4;     // K split over the waves
+constexpr int RT = 32;          // tile edge
+constexpr int RSPLIT = 8;       // K split over the waves of a workgroup
+constexpr int RTHREADS = 64 * RSPLIT;
 
 __device__ __forceinline__ const unsigned char *rec_state_row(const DevState &st, int r, int R, int rowbytes) {
   return state_row(st, min(r, R - 1), rowbytes);
 }
 
-__global__ __launch_bounds__(THREADS) void k_rec_f32(DevState st) {
+__global__ __launch_bounds__(RTHREADS) void k_rec_f32(DevState st) {
   const int R = st.ctrl->R;
   const int d = st.d;
   const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
@@ -56,12 +57,13 @@ __global__ __launch_bounds__(THREADS) void k_rec_f32(DevState st) {
   __shared__ float red[RSPLIT][RT * RT];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rowbytes = d * 4;
-  const int kq = d / RSPLIT;                       // K range of this wave
+  const int kq = d / RSPLIT;                       // K range of this wave (multiple of 8)
   const float *arow = static_cast<const float *>(st.W_h) + (size_t)(v0 + (lane & 31)) * d + w * kq;
   const float *brow = reinterpret_cast<const float *>(rec_state_row(st, r0 + (lane & 31), R, rowbytes)) + w * kq;
   const int h = (lane >> 5) * 4;
   f16v acc = {};
-#pragma unroll 4
+  // K permutation: lanes 0-31 feed k = kk + e, lanes 32-63 k = kk + 4 + e.
+#pragma unroll 8
   for (int kk = 0; kk < kq; kk += 8) {
     const f4 a = *reinterpret_cast<const f4 *>(arow + kk + h);
     const f4 b = *reinterpret_cast<const f4 *>(brow + kk + h);
@@ -75,20 +77,23 @@ __global__ __launch_bounds__(THREADS) void k_rec_f32(DevState st) {
     red[w][(lane & 31) * RT + i] = acc[reg];
   }
   __syncthreads();
-  // 256 threads x 4 outputs: thread -> row j = tid/8, features 4*(tid%8)..+3.
-  const int j = threadIdx.x >> 3, i0 = (threadIdx.x & 7) * 4;
+  // 512 threads x 2 outputs: thread -> row j = tid/16, features 2*(tid%16)..+1.
+  const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
   const int row = r0 + j;
   if (row >= R) return;
   const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
-  const f4 e = *reinterpret_cast<const f4 *>(E);
-  f4 hv;
+  float hv[2];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < 2; ++q) {
     const int o = j * RT + i0 + q;
-    const float pre = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
-    hv[q] = tanhf(pre + e[q]);
+    float pre = red[0][o];
+#pragma unroll
+    for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
+    hv[q] = tanhf(pre + E[q]);
   }
-  *reinterpret_cast<f4 *>(static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0) = hv;
+  float *out = static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0;
+  out[0] = hv[0];
+  out[1] = hv[1];
 }
 
 // bf16 states are rounded after tanh, a discontinuous map: any difference
@@ -96,7 +101,7 @@ __global__ __launch_bounds__(THREADS) void k_rec_f32(DevState st) {
 // Products of two bf16 values are exact in fp64 and so is their sum over
 // the state size in practice, so the pre-activation is accumulated with the
 // fp64 MFMA (16x16x4), tanh taken in fp64 and the result rounded once.
-__global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
+__global__ __launch_bounds__(RTHREADS) void k_rec_bf16(DevState st) {
   const int R = st.ctrl->R;
   const int d = st.d;
   const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
@@ -107,7 +112,7 @@ __global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
   __shared__ double red[RSPLIT][RT * RT];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rowbytes = d * 2;
-  const int kq = d / RSPLIT;
+  const int kq = d / RSPLIT;                       // multiple of 16
   const int r16 = lane & 15, g = lane >> 4;
   // A: 2 blocks of 16 out features, B: 2 blocks of 16 rows; the lane feeds
   // 4 consecutive bf16 at k = kk + 4g to 4 MFMAs (same permutation for A, B).
@@ -126,7 +131,7 @@ __global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
     o[2] = (double)__uint_as_float(raw[1] << 16);
     o[3] = (double)__uint_as_float(raw[1] & 0xFFFF0000u);
   };
-#pragma unroll 2
+#pragma unroll 4
   for (int kk = 0; kk < kq; kk += 16) {
     double a[2][4], b[2][4];
     cvt(*reinterpret_cast<const u2 *>(a0 + kk), a[0]);
@@ -153,24 +158,21 @@ __global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
         red[w][j * RT + i] = acc[x][y][q];
       }
   __syncthreads();
-  const int j = threadIdx.x >> 3, i0 = (threadIdx.x & 7) * 4;
+  const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
   const int row = r0 + j;
   if (row >= R) return;
   const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
-  const u2 eraw = *reinterpret_cast<const u2 *>(E);
-  double e[4];
-  cvt(eraw, e);
-  uint16_t hb[4];
+  uint16_t hb[2];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < 2; ++q) {
     const int o = j * RT + i0 + q;
-    const double pre = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
-    hb[q] = bf16_rne_from_double(tanh(pre + e[q]));
+    double pre = red[0][o];
+#pragma unroll
+    for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
+    hb[q] = bf16_rne_from_double(tanh(pre + (double)bf16f(E[q])));
   }
-  u2 packed;
-  packed[0] = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-  packed[1] = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
-  *reinterpret_cast<u2 *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) = packed;
+  *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) =
+      (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
 }
 
 }  // namespace
@@ -178,9 +180,9 @@ __global__ __launch_bounds__(THREADS) void k_rec_bf16(DevState st) {
 hipError_t launch_rec(const DevState &st, hipStream_t s) {
   const int G = xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT));
   if (st.dtype == 1)
-    hipLaunchKernelGGL(k_rec_bf16, dim3(G), dim3(THREADS), 0, s, st);
+    hipLaunchKernelGGL(k_rec_bf16, dim3(G), dim3(RTHREADS), 0, s, st);
   else
-    hipLaunchKernelGGL(k_rec_f32, dim3(G), dim3(THREADS), 0, s, st);
+    hipLaunchKernelGGL(k_rec_f32, dim3(G), dim3(RTHREADS), 0, s, st);
   return hipGetLastError();
 }
 

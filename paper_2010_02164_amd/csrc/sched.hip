@@ -55,93 +55,147 @@ __device__ int block_min(int v, int *sm) {
   return r;
 }
 
+// Each thread owns a contiguous range of at most SCHED_MAXB beams (so rows
+// come out in beam order) and keeps their records in registers; every
+// decision needs one block-wide scan or reduction.
+constexpr int SCHED_MAXB = 4;
+
+__device__ long long block_excl_scan64(long long v, long long *sm, long long *total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  long long x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const long long y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sm[w] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long long acc = 0;
+    for (int i = 0; i < nw; ++i) {
+      const long long t = sm[i];
+      sm[i] = acc;
+      acc += t;
+    }
+    sm[nw] = acc;
+  }
+  __syncthreads();
+  const long long res = sm[w] + x - v;
+  *total = sm[nw];
+  __syncthreads();
+  return res;
+}
+
 __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
+  __shared__ long long sm64[SCHED_THREADS / 64 + 1];
   __shared__ int sm[SCHED_THREADS / 64 + 1];
   DevCtrl *c = st.ctrl;
-  const int tid = threadIdx.x, nt = blockDim.x;
+  const int tid = threadIdx.x;
   const int n = st.n, k = st.k;
   const int nq = c->n_queued, cursor = c->cursor;
+  const int per = (n + SCHED_THREADS - 1) / SCHED_THREADS;   // <= SCHED_MAXB
+  const int b0 = min(n, tid * per), nb = min(n, b0 + per) - b0;
 
-  // Live beams before admission (|B| in Alg. 1).
-  int lc = 0;
-  for (int b = tid; b < n; b += nt) lc += (st.b_input[b] >= 0);
-  int live;
-  block_excl_scan(lc, sm, &live);
+  int inp[SCHED_MAXB], stp[SCHED_MAXB];
+  int live_l = 0;
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) {
+    inp[u] = -1;
+    stp[u] = 0;
+    if (u < nb) {
+      inp[u] = st.b_input[b0 + u];
+      stp[u] = st.b_steps[b0 + u];
+      live_l += inp[u] >= 0;
+    }
+  }
+  // One scan: live beams (low 32 bits) and free beams (high 32 bits).
+  long long tot;
+  const long long pre = block_excl_scan64(((long long)(nb - live_l) << 32) | live_l, sm64, &tot);
+  const int live = (int)(tot & 0xffffffff);
 
-  // Refill: if inputs remain and |B| <= eps*n, admit m = min(n - |B|, left)
-  // new inputs, in index order, into the free beam records in index order.
+  // Refill (Alg. 1): if inputs remain and |B| <= eps*n, admit
+  // m = min(n - |B|, left) new inputs, in index order, into the free beam
+  // records in index order.
   int admit = 0;
   if (cursor < nq && live <= st.refill_thr) admit = min(n - live, nq - cursor);
   if (admit > 0) {
-    const int per = (n + nt - 1) / nt;
-    const int b0 = min(n, tid * per), b1 = min(n, b0 + per);
-    int fc = 0;
-    for (int b = b0; b < b1; ++b) fc += (st.b_input[b] < 0);
-    int tot;
-    int rank = block_excl_scan(fc, sm, &tot);
-    for (int b = b0; b < b1; ++b) {
-      if (st.b_input[b] >= 0) continue;
-      if (rank < admit) {
-        st.b_input[b] = cursor + rank;
-        st.b_steps[b] = 0;
-        st.b_par[b] = 0;
-        for (int j = 0; j < k; ++j) {
-          st.s_status[b * k + j] = j == 0 ? SLOT_ACTIVE : SLOT_EMPTY;
-          st.s_score[b * k + j] = 0.0;
-          st.s_tok[b * k + j] = 0;   // start symbol
+    int rank = (int)(pre >> 32);
+#pragma unroll
+    for (int u = 0; u < SCHED_MAXB; ++u) {
+      if (u < nb && inp[u] < 0) {
+        if (rank < admit) {
+          const int b = b0 + u;
+          inp[u] = cursor + rank;
+          stp[u] = 0;
+          st.b_input[b] = inp[u];
+          st.b_steps[b] = 0;
+          st.b_par[b] = 0;
+          for (int j = 0; j < k; ++j) {
+            st.s_status[b * k + j] = j == 0 ? SLOT_ACTIVE : SLOT_EMPTY;
+            st.s_score[b * k + j] = 0.0;
+            st.s_tok[b * k + j] = 0;   // start symbol
+          }
         }
+        ++rank;
       }
-      ++rank;
     }
   }
-  __syncthreads();
 
   // Selection: the live beams with the fewest steps taken.
-  int mn = INT_MAX;
-  for (int b = tid; b < n; b += nt)
-    if (st.b_input[b] >= 0) mn = min(mn, st.b_steps[b]);
-  mn = block_min(mn, sm);
+  int mn_l = INT_MAX;
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u)
+    if (u < nb && inp[u] >= 0) mn_l = min(mn_l, stp[u]);
+  const int mn = block_min(mn_l, sm);
 
-  // Compaction of the selected beams' active candidates, in slot order.
-  const int nslots = n * k;
-  const int per = (nslots + nt - 1) / nt;
-  const int s0 = min(nslots, tid * per), s1 = min(nslots, s0 + per);
-  int ac = 0, tc = 0;
-  for (int s = s0; s < s1; ++s) {
-    const int b = s / k;
-    const bool sel = st.b_input[b] >= 0 && st.b_steps[b] == mn;
-    const int status = st.s_status[s];
-    ac += (sel && status == SLOT_ACTIVE);
-    tc += (sel && (status == SLOT_EOS || status == SLOT_MAXLEN));
-  }
-  int R;
-  int row = block_excl_scan(ac, sm, &R);
-  int noops;
-  block_excl_scan(tc, sm, &noops);
-  for (int s = s0; s < s1; ++s) {
-    const int b = s / k;
-    const bool sel = st.b_input[b] >= 0 && st.b_steps[b] == mn;
-    if (sel && st.s_status[s] == SLOT_ACTIVE) {
-      const int q = st.b_input[b];
-      st.r_slot[row] = s;
-      st.r_hsrc[row] = mn == 0 ? -1 - q : s;   // a fresh beam reads its encoding h0
-      st.r_y[row] = st.s_tok[s];
-      st.r_t[row] = mn + 1;
-      st.r_Lx[row] = st.q_Lx[q];
-      st.s_row[s] = row;
-      ++row;
-    } else {
-      st.s_row[s] = -1;
+  // Active and terminated candidates of the selected beams (slot order);
+  // each beam's active slots are kept as a bit mask.
+  int act_l = 0, term_l = 0, sel_l = 0;
+  uint32_t amask[SCHED_MAXB];
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) {
+    amask[u] = 0u;
+    const bool sel = u < nb && inp[u] >= 0 && stp[u] == mn;
+    sel_l += sel;
+    if (sel) {
+      for (int j = 0; j < k; ++j) {
+        const int status = st.s_status[(b0 + u) * k + j];
+        amask[u] |= (uint32_t)(status == SLOT_ACTIVE) << j;
+        term_l += status == SLOT_EOS || status == SLOT_MAXLEN;
+      }
+      act_l += __popc(amask[u]);
     }
   }
-  int ns = 0;
-  for (int b = tid; b < n; b += nt) {
-    const int sel = st.b_input[b] >= 0 && st.b_steps[b] == mn;
-    st.b_sel[b] = sel;
-    ns += sel;
+  long long tot2;
+  const long long pre2 = block_excl_scan64(((long long)term_l << 32) | act_l, sm64, &tot2);
+  const int R = (int)(tot2 & 0xffffffff);
+  const int noops = (int)(tot2 >> 32);
+  int row = (int)(pre2 & 0xffffffff);
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) {
+    if (u < nb) {
+      const int b = b0 + u;
+      const bool sel = inp[u] >= 0 && stp[u] == mn;
+      st.b_sel[b] = sel;
+      const int lx = sel ? st.q_Lx[inp[u]] : 0;
+      for (int j = 0; j < k; ++j) {
+        const int s = b * k + j;
+        if ((amask[u] >> j) & 1u) {
+          st.r_slot[row] = s;
+          st.r_hsrc[row] = mn == 0 ? -1 - inp[u] : s;   // a fresh beam reads its encoding h0
+          st.r_y[row] = st.s_tok[s];
+          st.r_t[row] = mn + 1;
+          st.r_Lx[row] = lx;
+          st.s_row[s] = row;
+          ++row;
+        } else {
+          st.s_row[s] = -1;
+        }
+      }
+    }
   }
   int nsel;
-  block_excl_scan(ns, sm, &nsel);
+  block_excl_scan(sel_l, sm, &nsel);
 
   if (tid == 0) {
     c->cursor = cursor + admit;
