@@ -20,8 +20,10 @@ oracle timed on this host's cores on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -31,6 +33,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA, MI355X
+# Sources of the projection kernel; measured HBM traffic is reported only
+# while they are unchanged since the counters were taken.
+PROJ_SOURCES = ["paper_2010_02164_amd/csrc/proj.hip", "paper_2010_02164_amd/csrc/topk.h",
+                "paper_2010_02164_amd/csrc/mfma_common.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_proj_traffic.md")
 METRIC = "finalized hyps/sec + expansions/sec (Var-Stream, k=5, |V|=32k), % roofline"
 
 
@@ -60,6 +67,41 @@ def cpu_baseline(wl, sched, eps, sample):
             "expansions_per_s": r.expansions / dt, "seconds": dt}
 
 
+def proj_source_sha256():
+    h = hashlib.sha256()
+    for rel in PROJ_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload_key):
+    """HBM bytes per projection launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, calibrated against a plain copy), or None when
+    that summary is for another workload or an older kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    for block in re.findall(r"```json\n(.*?)\n```", text, re.S):
+        rec = json.loads(block)
+        if rec.get("workload_key") == workload_key and rec.get("source_sha256") == proj_source_sha256():
+            return rec["hbm_bytes_per_launch"]
+    return None
+
+
+def copy_calibration(nbytes, reps=5):
+    """A plain device copy of a known size, for scaling the HBM byte counters."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -70,11 +112,19 @@ def main():
     ap.add_argument("--eps", type=float, default=None)
     ap.add_argument("--cpu-sample", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph-replay", action="store_true",
+                    help="skip the extra untimed graph-replay decodes (counter runs)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               "(inputs are independent: shard them over GPUs, one decoder per GPU)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
     from paper_2010_02164_amd import decoder_for_workload, inputs_to_device, weights_to_device
@@ -115,12 +165,14 @@ def main():
     assert len(hyps) == st["hyps"]
 
     # The same workload replayed as captured step graphs, untimed kernels.
-    torch.cuda.synchronize()
-    t2 = time.perf_counter()
-    for _ in range(args.steps):
-        run_once()
-    torch.cuda.synchronize()
-    graph_per_run = (time.perf_counter() - t2) / args.steps
+    graph_per_run = None
+    if not args.no_graph_replay:
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        for _ in range(args.steps):
+            run_once()
+        torch.cuda.synchronize()
+        graph_per_run = (time.perf_counter() - t2) / args.steps
 
     per_run = elapsed / args.steps
     hyps_per_s = st["hyps"] / per_run
@@ -129,23 +181,24 @@ def main():
     proj_flops = 2.0 * cfg.d * cfg.V * st["expansions"] * args.steps
     achieved = proj_flops / (proj_ms * 1e-3) / 1e12 if proj_ms > 0 else 0.0
     peak = PEAK_TFLOPS[cfg.dtype]
+    workload_key = f"cfg{args.config} {args.sched} eps={eps:g}"
     out = {
         "metric": METRIC, "value": hyps_per_s, "unit": "hyps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": per_run * 1e3,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": _workload_desc(cfg, args.sched, eps), "inputs": N,
+        "config": {"workload": _workload_desc(cfg, args.sched, eps), "key": workload_key, "inputs": N,
                    "parallelism": "single GPU"},
         "expansions_per_s": exps_per_s,
         "search": {k: st[k] for k in ("timesteps", "expansions", "noops", "refills", "hyps")},
         "roofline": {"bound": "mfma", "kernel": "k_proj (vocabulary projection + log-sum-exp + top-k)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None, "launches": proj_launches,
+                     "traffic": measured_traffic(workload_key), "launches": proj_launches,
                      "avg_launch_us": proj_ms * 1e3 / max(proj_launches, 1)},
         "rows_per_step_hist": {"bucket_width": hist_w,
                                "counts": {str(i * hist_w): c for i, c in enumerate(hist) if c}},
         "projection_share_of_step": (proj_ms * 1e-3) / elapsed if elapsed > 0 else None,
-        "graph_replay_hyps_per_s": st["hyps"] / graph_per_run,
+        "graph_replay_hyps_per_s": st["hyps"] / graph_per_run if graph_per_run else None,
         "collect_d2h_ms": collect_s * 1e3,
         "pcie_inclusive_hyps_per_s": st["hyps"] / (per_run + collect_s),
     }
