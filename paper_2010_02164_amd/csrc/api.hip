@@ -325,6 +325,15 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.max_inputs = p.max_inputs;
   st.kbucket = kbucket_of(p.k);
   st.hist_width = std::max(16, (st.R_max + 63) / 64);
+  {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0) {
+      sb_destroy(dec);
+      return SB_E_HIP;
+    }
+    st.n_cu = ncu;
+  }
   st.delta = p.delta;
   st.beta = model->eos_beta;
 

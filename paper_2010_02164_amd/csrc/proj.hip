@@ -4,174 +4,209 @@
 // The R x |V| logits never reach memory: each workgroup writes, per row and
 // 128-wide vocabulary tile, (max, sum exp) and its best kb (value, token).
 //
-// Workgroup: 4 waves, tile 128 vocabulary rows (32 per wave) x 128 batch rows
-// (4 blocks of 32). W_out, the large streamed operand, is kept 3 K-chunks
-// ahead in registers (48 KB in flight per workgroup) to cover HBM/MALL
-// latency, and both operands pass through a double-buffered LDS tile so
-// that global loads stay fully coalesced. Blocks of 32 rows past R are
-// skipped, so small steps cost proportionally less. The K loop runs in 128-byte
-// chunks per row; every output accumulates over K in the same fixed order
-// whatever rows share the step, so a row's results do not depend on the batch.
+// Workgroup: 8 waves on a tile of 128 vocabulary rows x 128 batch rows (4
+// blocks of 32). The K range is split in two fixed halves: waves 0-3 sum the
+// first half, waves 4-7 the second, each wave over its own 32 vocabulary
+// rows; the two partial sums are added once at the end. Every output
+// therefore accumulates in the same order whatever rows share the step, so a
+// row's result does not depend on the batch.
+//
+// W_out is streamed straight into registers from a copy laid out in MFMA
+// fragment order (one coalesced 1 KB load per wave and fragment), kept D
+// chunks ahead; the states of each half pass through a double-buffered LDS
+// tile shared by its four waves, loaded D chunks ahead as well. Blocks of 32
+// rows past R are neither loaded nor computed.
+#include <algorithm>
+
 #include "mfma_common.h"
 #include "topk.h"
 
 namespace sb {
 namespace {
 
-constexpr int THREADS = 256;
+constexpr int THREADS = 512;
 constexpr int NB = 4;            // 32-row batch blocks per workgroup
 constexpr int TR = 32 * NB;      // batch rows per workgroup
 constexpr int TV = GEMM_BV;      // vocabulary rows per workgroup (4 waves x 32)
 constexpr int CH = 128;          // bytes of a row's K chunk
 constexpr int LS = CH + 16;      // padded LDS row stride (bytes)
-constexpr int AD = 3;            // W_out prefetch depth (chunks)
+constexpr int FRAG = 1024;       // bytes of one wave-wide 16-byte-per-lane fragment
+constexpr int WCH = 4 * FRAG;    // bytes of one wave's W_out fragments per chunk
+constexpr int D = 3;             // prefetch depth (chunks)
 
 template <int KB>
 union ProjSmem {
-  struct {
-    unsigned char A[2][TV][LS];
-    unsigned char B[2][TR][LS];
-  } t;
-  float xch[4][TR][2 + 2 * KB];
+  unsigned char B[2][2][TR][LS];          // [buffer][K half][row][byte]
+  float red[2][4][2][16][64];             // [sending half][slice][block][reg][lane]
+  float xch[4][TR][2 + 2 * KB];           // [slice][row][max, sumexp, keys]
 };
 
-// K loop of one workgroup: acc[b] (b < NBV) += W_out tile x batch block b.
-// Both operands are staged through a double-buffered LDS tile with fully
-// coalesced loads (8 lanes per 128-byte row segment): W_out through a
-// 3-chunk register prefetch ring, the states one chunk ahead. Loads return in
-// issue order, so each iteration issues them in the order they are consumed
-// (states chunk kt+2, then W_out chunk kt+4); prefetch indices are clamped
-// instead of guarded, so no load sits inside a branch.
+// K loop of one wave over its half: acc[b] (b < NBV) += W_out fragment x
+// batch block b. Chunk c of the half: W_out fragments at abase + c * 16 KB
+// (+ lane * 16 + q * 1 KB), the half's state tile at bbase + c * 128 bytes
+// (+ boff[u]). Loads of a chunk are issued together, D chunks ahead of use,
+// at indices clamped to the last chunk so that no load sits in a branch.
 template <bool BF16, int NBV>
-__device__ __forceinline__ void proj_mainloop(unsigned char (*A)[TV][LS], unsigned char (*B)[TR][LS],
-                                              const unsigned char *abase, const uint32_t *aoff,
-                                              const unsigned char *bbase, const uint32_t *boff,
-                                              int srow, int scol, int nk, int w, int l32, int h, f16v *acc) {
-  u4 as[AD][4];
-  u4 bs[4];
-  // Uniform base + 32-bit per-lane offset (SGPR-based addressing); chunk
-  // stride `cs` bytes (tiled W_out: one 16 KB block per chunk).
-  auto load = [&](const unsigned char *base, const uint32_t *off, uint32_t cs, int kt, u4 *dst) {
+__device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned char (*Bt1)[LS],
+                                              const unsigned char *abase, uint32_t alane,
+                                              const unsigned char *bbase, const uint32_t *boff, int srow,
+                                              int scol, int nh, int l32, int h, f16v *acc) {
+  u4 a[D][4];
+  u4 b[D][NBV];
+  auto loadA = [&](int c, u4 *dst) {
+    const unsigned char *p = abase + (uint32_t)c * (uint32_t)(4 * WCH);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) dst[u] = *reinterpret_cast<const u4 *>(base + (off[u] + (uint32_t)kt * cs));
+    for (int q = 0; q < 4; ++q) dst[q] = *reinterpret_cast<const u4 *>(p + alane + q * FRAG);
   };
-  auto store = [&](unsigned char (*T)[LS], const u4 *src) {
+  auto loadB = [&](int c, u4 *dst) {
+    const unsigned char *p = bbase + (uint32_t)c * CH;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) *reinterpret_cast<u4 *>(&T[srow + 32 * u][scol]) = src[u];
+    for (int u = 0; u < NBV; ++u) dst[u] = *reinterpret_cast<const u4 *>(p + boff[u]);
   };
-  auto compute = [&](int buf) {
+  auto storeB = [&](unsigned char (*T)[LS], const u4 *src) {
+#pragma unroll
+    for (int u = 0; u < NBV; ++u) *reinterpret_cast<u4 *>(&T[srow + 32 * u][scol]) = src[u];
+  };
+  auto compute = [&](unsigned char (*T)[LS], const u4 *af) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       // K permutation: lane half h at piece q feeds k = chunk + 16h + 4q + e
       // (fp32) or chunk + 32h + 8q + e (bf16), identically for both operands.
-      const u4 araw = *reinterpret_cast<const u4 *>(&A[buf][32 * w + l32][64 * h + 16 * q]);
       u4 braw[NBV];
 #pragma unroll
-      for (int b = 0; b < NBV; ++b) braw[b] = *reinterpret_cast<const u4 *>(&B[buf][32 * b + l32][64 * h + 16 * q]);
+      for (int bb = 0; bb < NBV; ++bb) braw[bb] = *reinterpret_cast<const u4 *>(&T[32 * bb + l32][64 * h + 16 * q]);
 #pragma unroll
-      for (int b = 0; b < NBV; ++b) {
+      for (int bb = 0; bb < NBV; ++bb) {
         if constexpr (BF16) {
-          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, araw),
-                                                           __builtin_bit_cast(bf8, braw[b]), acc[b], 0, 0, 0);
+          acc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, af[q]),
+                                                            __builtin_bit_cast(bf8, braw[bb]), acc[bb], 0, 0, 0);
         } else {
-          const f4 av = __builtin_bit_cast(f4, araw);
-          const f4 bv = __builtin_bit_cast(f4, braw[b]);
+          const f4 av = __builtin_bit_cast(f4, af[q]);
+          const f4 bv = __builtin_bit_cast(f4, braw[bb]);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], acc[b], 0, 0, 0);
+          for (int e = 0; e < 4; ++e) acc[bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], acc[bb], 0, 0, 0);
         }
       }
     }
   };
 
-  // Prologue: chunk 0 in LDS; states 1 and W_out 1, 2, 3 in flight.
-  load(bbase, boff, CH, 0, bs);
+  // Loads complete in issue order, so a wait for one chunk's states also
+  // waits for every load issued before them: the scheduling fences keep the
+  // issue order chunk by chunk (W_out, then states), which leaves D-1 chunks
+  // in flight at every wait.
+  // Prologue: chunks 0 .. D-1 in flight, chunk 0's states in LDS.
 #pragma unroll
-  for (int c = 0; c < AD; ++c) load(abase, aoff, TV * CH, min(c, nk - 1), as[c]);
-  store(A[0], as[0]);
-  store(B[0], bs);
-  load(bbase, boff, CH, min(1, nk - 1), bs);
-  load(abase, aoff, TV * CH, min(AD, nk - 1), as[0]);
+  for (int c = 0; c < D; ++c) {
+    loadA(min(c, nh - 1), a[c]);
+    __builtin_amdgcn_sched_barrier(0);
+    loadB(min(c, nh - 1), b[c]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  storeB(Bt, b[0]);
   __syncthreads();
 
-  for (int kt0 = 0; kt0 < nk; kt0 += AD) {
+  for (int i0 = 0; i0 < nh; i0 += D) {
 #pragma unroll
-    for (int j = 0; j < AD; ++j) {
-      const int kt = kt0 + j;   // kt % AD == j
-      if (kt < nk) compute(kt & 1);
-      // W_out chunk kt+1 sits in as[(kt+1)%AD], states chunk kt+1 in bs.
-      if (kt + 1 < nk) {
-        store(A[(kt + 1) & 1], as[(j + 1) % AD]);
-        store(B[(kt + 1) & 1], bs);
-      }
-      load(bbase, boff, CH, min(kt + 2, nk - 1), bs);
-      load(abase, aoff, TV * CH, min(kt + 1 + AD, nk - 1), as[(j + 1) % AD]);
+    for (int j = 0; j < D; ++j) {
+      const int i = i0 + j;   // i % D == j
+      if (i < nh) compute((i & 1) ? Bt1 : Bt, a[j]);
+      __builtin_amdgcn_sched_barrier(0);
+      // States of chunk i+1 sit in b[(j+1) % D]; buffer (i+1)&1 was last
+      // read before the previous barrier.
+      if (i + 1 < nh) storeB(((i + 1) & 1) ? Bt1 : Bt, b[(j + 1) % D]);
+      __builtin_amdgcn_sched_barrier(0);
+      loadA(min(i + D, nh - 1), a[j]);
+      __builtin_amdgcn_sched_barrier(0);
+      loadB(min(i + D, nh - 1), b[j]);
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
     }
   }
 }
 
+// One 128 x 128 output tile (vocabulary tile vt, batch tile rt).
 template <bool BF16, int KB>
-__global__ __launch_bounds__(THREADS, 2) void k_proj(DevState st) {
-  const int R = st.ctrl->R;
+__device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, int vt, int rt, int R) {
   const int d = st.d, V = st.V;
-  const int nvt = st.S, nrt = (st.R_max + TR - 1) / TR;
-  int vt, rt;
-  if (!tile_of(nvt, nrt, vt, rt)) return;
   const int v0 = vt * TV, r0 = rt * TR;
-  if (r0 >= R) return;
   const int nbv = min(NB, (R - r0 + 31) >> 5);    // blocks holding valid rows
-  __shared__ ProjSmem<KB> sm;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = w >> 2, wv = w & 3;               // K half, vocabulary slice
   const int l32 = lane & 31, h = lane >> 5;
   const int rowbytes = d * (BF16 ? 2 : 4);
-  const int nk = rowbytes / CH;
+  const int nk = rowbytes / CH;                   // even: d is a multiple of 64 (fp32) / 128 (bf16)
+  const int nh = nk >> 1;
+  const int kbeg = g * nh;
 
-  // Staging: thread -> rows (tid/8) + 32u, 16-byte column tid%8, of the
-  // W_out tile (a contiguous 16 KB block per K chunk in the tiled copy) and
-  // of the state tile (batch rows, clamped to R-1). Chunk kt of W_out sits
-  // kt * 16 KB further; of the states, kt * 128 bytes further.
-  const int srow = tid >> 3, scol = (tid & 7) * 16;
-  // Byte offsets fit 32 bits (the tiled W_out is checked at create time).
-  uint32_t aoff[4], boff[4];
+  // W_out fragments of this wave: chunk kt at ((vt*nk + kt)*4 + wv) * 4 KB.
+  const unsigned char *abase = st.wout_t + ((size_t)(vt * nk + kbeg) * 4 + wv) * WCH;
+  // State staging: thread -> rows (tg/8) + 32u of the tile (clamped to R-1),
+  // 16-byte column tg%8 of the half's chunk.
+  const int tg = tid & 255;
+  const int srow = tg >> 3, scol = (tg & 7) * 16;
+  uint32_t boff[NB];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    aoff[u] = ((uint32_t)vt * (uint32_t)nk * TV + srow + 32 * u) * CH + scol;
-    boff[u] = (uint32_t)min(r0 + srow + 32 * u, R - 1) * (uint32_t)rowbytes + scol;
-  }
-  const unsigned char *abase = st.wout_t;
-  const unsigned char *bbase = static_cast<const unsigned char *>(st.hbuf);
+  for (int u = 0; u < NB; ++u) boff[u] = (uint32_t)min(r0 + srow + 32 * u, R - 1) * (uint32_t)rowbytes + scol;
+  const unsigned char *bbase = static_cast<const unsigned char *>(st.hbuf) + (size_t)kbeg * CH;
   f16v acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f16v{};
   // One mainloop instantiation per count of valid 32-row blocks, so the
   // K loop has no per-block branches.
+  unsigned char (*Bt)[LS] = sm.B[0][g];
+  unsigned char (*Bt1)[LS] = sm.B[1][g];
+  const uint32_t alane = (uint32_t)lane * 16u;
   switch (nbv) {
-    case 1: proj_mainloop<BF16, 1>(sm.t.A, sm.t.B, abase, aoff, bbase, boff, srow, scol, nk, w, l32, h, acc); break;
-    case 2: proj_mainloop<BF16, 2>(sm.t.A, sm.t.B, abase, aoff, bbase, boff, srow, scol, nk, w, l32, h, acc); break;
-    case 3: proj_mainloop<BF16, 3>(sm.t.A, sm.t.B, abase, aoff, bbase, boff, srow, scol, nk, w, l32, h, acc); break;
-    default: proj_mainloop<BF16, 4>(sm.t.A, sm.t.B, abase, aoff, bbase, boff, srow, scol, nk, w, l32, h, acc); break;
+    case 1: proj_mainloop<BF16, 1>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    case 2: proj_mainloop<BF16, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    case 3: proj_mainloop<BF16, 3>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    default: proj_mainloop<BF16, 4>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
   }
 
-  // Epilogue. Block b: lane holds batch row r0 + 32b + l32 and the wave's
-  // vocabulary rows v0 + 32w + 8*(reg/4) + 4h + reg%4, increasing with reg.
-  constexpr int PW = 2 + 2 * KB;
-  float bias_row[NB];
+  // Combine the halves. Half g owns blocks 2g and 2g+1: it sends its sums of
+  // the other half's blocks through LDS and adds the received ones to its own
+  // (one addition per output, commutative, so the order is fixed).
+  f16v own[2], snd[2];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    const int j = r0 + 32 * b + l32;
-    bias_row[b] = (v0 == 0 && j < R) ? st.beta * (float)(st.r_t[j] - st.r_Lx[j]) : 0.0f;
+  for (int bl = 0; bl < 2; ++bl) {
+    own[bl] = g ? acc[2 + bl] : acc[bl];
+    snd[bl] = g ? acc[bl] : acc[2 + bl];
   }
-  TopK<KB> tks[NB];
-  float ms[NB], ss[NB];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    if (b < nbv) {
+  for (int bl = 0; bl < 2; ++bl) {
+    if (2 * (1 - g) + bl < nbv) {
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) sm.red[g][wv][bl][reg][lane] = snd[bl][reg];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int bl = 0; bl < 2; ++bl) {
+    if (2 * g + bl < nbv) {
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) own[bl][reg] += sm.red[1 - g][wv][bl][reg][lane];
+    }
+  }
+
+  // Epilogue on the owned blocks. Block 2g+bl: lane holds batch row
+  // r0 + 32(2g+bl) + l32 and the wave's vocabulary rows
+  // v0 + 32wv + 8*(reg/4) + 4h + reg%4, increasing with reg.
+  constexpr int PW = 2 + 2 * KB;
+  TopK<KB> tks[2];
+  float ms[2], ss[2];
+#pragma unroll
+  for (int bl = 0; bl < 2; ++bl) {
+    const int blk = 2 * g + bl;
+    if (blk < nbv) {
+      const int j = r0 + 32 * blk + l32;
+      const float bias = (v0 == 0 && j < R) ? st.beta * (float)(st.r_t[j] - st.r_Lx[j]) : 0.0f;
       float vals[16];
 #pragma unroll
       for (int reg = 0; reg < 16; ++reg) {
-        const int v = v0 + 32 * w + 8 * (reg >> 2) + 4 * h + (reg & 3);
-        float z = acc[b][reg];
-        if (v == 0) z += bias_row[b];
+        const int v = v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3);
+        float z = own[bl][reg];
+        if (v == 0) z += bias;
         vals[reg] = v < V ? z : -INFINITY;
       }
       float m = -INFINITY;
@@ -186,31 +221,32 @@ __global__ __launch_bounds__(THREADS, 2) void k_proj(DevState st) {
       cand_key keys[16];
 #pragma unroll
       for (int reg = 0; reg < 16; ++reg)
-        keys[reg] = make_key(vals[reg], v0 + 32 * w + 8 * (reg >> 2) + 4 * h + (reg & 3));
+        keys[reg] = make_key(vals[reg], v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3));
       bitonic_sort_desc<16>(keys);
 #pragma unroll
-      for (int q = 0; q < KB; ++q) tks[b].k[q] = keys[q];
+      for (int q = 0; q < KB; ++q) tks[bl].k[q] = keys[q];
       TopK<KB> o;
-      topk_shfl_xor(o, tks[b], 32);
+      topk_shfl_xor(o, tks[bl], 32);
       const float m2 = __shfl_xor(m, 32, 64), s2 = __shfl_xor(s, 32, 64);
       lse_merge(m, s, m2, s2);
-      topk_merge(tks[b], o);
-      ms[b] = m;
-      ss[b] = s;
+      topk_merge(tks[bl], o);
+      ms[bl] = m;
+      ss[bl] = s;
     }
   }
-  // The staging tile is dead after the last barrier of the K loop.
+  __syncthreads();   // the exchange area is reused below
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    if (b < nbv && lane < 32) {
-      float *p = sm.xch[w][32 * b + l32];
-      p[0] = ms[b];
-      p[1] = ss[b];
-      topk_store(p + 2, tks[b]);
+  for (int bl = 0; bl < 2; ++bl) {
+    const int blk = 2 * g + bl;
+    if (blk < nbv && lane < 32) {
+      float *p = sm.xch[wv][32 * blk + l32];
+      p[0] = ms[bl];
+      p[1] = ss[bl];
+      topk_store(p + 2, tks[bl]);
     }
   }
   __syncthreads();
-  // Wave w merges the four vocabulary quarters of batch block w.
+  // Wave w < 4 merges the four vocabulary slices of batch block w.
   if (w < nbv && lane < 32) {
     const int row = 32 * w + l32;
     const int j = r0 + row;
@@ -234,28 +270,61 @@ __global__ __launch_bounds__(THREADS, 2) void k_proj(DevState st) {
   }
 }
 
-// W_out [V][d] -> tiled [S][nk][128][128 bytes], zero rows past V.
+// Persistent launch: at most one workgroup per compute unit, each walking
+// its share of the active tiles (vocabulary tile major, batch tile minor).
+// Workgroup ids are dealt round robin to the 8 XCDs; XCD x takes the x-th
+// eighth of the tile list, so the batch tiles of one vocabulary tile run
+// side by side on one XCD and share its L2 copy of the W_out tile. Rounds
+// alternate direction over the XCD's workgroups, so that a workgroup which
+// drew a full batch tile in one round draws a partial one in the next. Only
+// tiles holding rows of this step are visited, and no workgroup is launched
+// just to exit (idle ones would occupy compute units that the dispatcher
+// then withholds from working ones).
+template <bool BF16, int KB>
+__global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
+  const int R = st.ctrl->R;
+  if (R <= 0) return;
+  const int nra = (R + TR - 1) / TR;
+  const int T = st.S * nra;
+  const int x = blockIdx.x & 7, gx = gridDim.x >> 3, j = blockIdx.x >> 3;
+  const int lo = (int)((long long)T * x / 8), nt = (int)((long long)T * (x + 1) / 8) - lo;
+  __shared__ ProjSmem<KB> sm;
+  for (int r = 0; r * gx < nt; ++r) {
+    const int idx = (r & 1) ? (r + 1) * gx - 1 - j : r * gx + j;
+    if (idx >= nt) continue;
+    const int tile = lo + idx;
+    const int vt = tile / nra, rt = tile - vt * nra;
+    proj_tile<BF16, KB>(st, sm, vt, rt, R);
+    __syncthreads();   // LDS is reused by the next tile
+  }
+}
+
+// W_out [V][d] -> MFMA fragment order [S][nk][4 slices][4 pieces][64 lanes][16 B]:
+// lane (h, l) of slice s at piece q holds bytes kt*128 + 64h + 16q .. +15 of
+// vocabulary row 128*vt + 32s + l (zero past V).
 __global__ void k_relayout_wout(const unsigned char *__restrict__ src, unsigned char *__restrict__ dst, int V,
                                 int rowbytes, int S) {
   const int nk = rowbytes / CH;
-  const size_t pieces = (size_t)S * nk * TV * (CH / 16);
+  const size_t pieces = (size_t)S * nk * 4 * 4 * 64;
   for (size_t p = (size_t)blockIdx.x * blockDim.x + threadIdx.x; p < pieces; p += (size_t)gridDim.x * blockDim.x) {
-    const int piece = (int)(p % (CH / 16));
-    const size_t rowblk = p / (CH / 16);          // ((vt * nk + kt) * TV + row)
-    const int row = (int)(rowblk % TV);
-    const size_t vk = rowblk / TV;
+    const int ln = (int)(p & 63);
+    const int q = (int)((p >> 6) & 3);
+    const int s = (int)((p >> 8) & 3);
+    const size_t vk = p >> 10;                  // vt * nk + kt
     const int kt = (int)(vk % nk);
     const int vt = (int)(vk / nk);
-    const int v = vt * TV + row;
+    const int v = vt * TV + 32 * s + (ln & 31);
     u4 val = {0u, 0u, 0u, 0u};
-    if (v < V) val = *reinterpret_cast<const u4 *>(src + (size_t)v * rowbytes + (size_t)kt * CH + piece * 16);
+    if (v < V)
+      val = *reinterpret_cast<const u4 *>(src + (size_t)v * rowbytes + (size_t)kt * CH + 64 * (ln >> 5) + 16 * q);
     *reinterpret_cast<u4 *>(dst + p * 16) = val;
   }
 }
 
 template <bool BF16>
 hipError_t launch_proj_t(const DevState &st, hipStream_t s) {
-  const int G = xcd_grid(st.S * ((st.R_max + TR - 1) / TR));
+  // Multiple of 8, at most one per compute unit, no more than the tiles of a full step.
+  const int G = std::max(8, std::min(st.n_cu / 8 * 8, xcd_grid(st.S * ((st.R_max + TR - 1) / TR))));
   switch (st.kbucket) {
     case 4: hipLaunchKernelGGL((k_proj<BF16, 4>), dim3(G), dim3(THREADS), 0, s, st); break;
     case 8: hipLaunchKernelGGL((k_proj<BF16, 8>), dim3(G), dim3(THREADS), 0, s, st); break;

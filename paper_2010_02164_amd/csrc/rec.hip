@@ -2,6 +2,9 @@
 //   h = tanh(W_h h_prev + E[y])      [R,d] x [d,d]^T, fused epilogue
 // W_h (out-feature rows) is the MFMA A operand and the previous states the B
 // operand, both K-contiguous. bf16 workloads accumulate in fp64 (see k_rec_bf16).
+#include <algorithm>
+#include <type_traits>
+
 #include "mfma_common.h"
 
 namespace sb {
@@ -46,15 +49,9 @@ __device__ __forceinline__ const unsigned char *rec_state_row(const DevState &st
   return state_row(st, min(r, R - 1), rowbytes);
 }
 
-__global__ __launch_bounds__(RTHREADS) void k_rec_f32(DevState st) {
-  const int R = st.ctrl->R;
+__device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT * RT], int vt, int rt, int R) {
   const int d = st.d;
-  const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
-  int vt, rt;
-  if (!tile_of(nvt, nrt, vt, rt)) return;
   const int v0 = vt * RT, r0 = rt * RT;
-  if (r0 >= R) return;
-  __shared__ float red[RSPLIT][RT * RT];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rowbytes = d * 4;
   const int kq = d / RSPLIT;                       // K range of this wave (multiple of 8)
@@ -80,20 +77,21 @@ __global__ __launch_bounds__(RTHREADS) void k_rec_f32(DevState st) {
   // 512 threads x 2 outputs: thread -> row j = tid/16, features 2*(tid%16)..+1.
   const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
   const int row = r0 + j;
-  if (row >= R) return;
-  const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
-  float hv[2];
+  if (row < R) {
+    const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+    float hv[2];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int o = j * RT + i0 + q;
-    float pre = red[0][o];
+    for (int q = 0; q < 2; ++q) {
+      const int o = j * RT + i0 + q;
+      float pre = red[0][o];
 #pragma unroll
-    for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
-    hv[q] = tanhf(pre + E[q]);
+      for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
+      hv[q] = tanhf(pre + E[q]);
+    }
+    float *out = static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0;
+    out[0] = hv[0];
+    out[1] = hv[1];
   }
-  float *out = static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0;
-  out[0] = hv[0];
-  out[1] = hv[1];
 }
 
 // bf16 states are rounded after tanh, a discontinuous map: any difference
@@ -101,15 +99,9 @@ __global__ __launch_bounds__(RTHREADS) void k_rec_f32(DevState st) {
 // Products of two bf16 values are exact in fp64 and so is their sum over
 // the state size in practice, so the pre-activation is accumulated with the
 // fp64 MFMA (16x16x4), tanh taken in fp64 and the result rounded once.
-__global__ __launch_bounds__(RTHREADS) void k_rec_bf16(DevState st) {
-  const int R = st.ctrl->R;
+__device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[RT * RT], int vt, int rt, int R) {
   const int d = st.d;
-  const int nvt = d / RT, nrt = (st.R_max + RT - 1) / RT;
-  int vt, rt;
-  if (!tile_of(nvt, nrt, vt, rt)) return;
   const int v0 = vt * RT, r0 = rt * RT;
-  if (r0 >= R) return;
-  __shared__ double red[RSPLIT][RT * RT];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rowbytes = d * 2;
   const int kq = d / RSPLIT;                       // multiple of 16
@@ -160,29 +152,53 @@ __global__ __launch_bounds__(RTHREADS) void k_rec_bf16(DevState st) {
   __syncthreads();
   const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
   const int row = r0 + j;
-  if (row >= R) return;
-  const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
-  uint16_t hb[2];
+  if (row < R) {
+    const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+    uint16_t hb[2];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int o = j * RT + i0 + q;
-    double pre = red[0][o];
+    for (int q = 0; q < 2; ++q) {
+      const int o = j * RT + i0 + q;
+      double pre = red[0][o];
 #pragma unroll
-    for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
-    hb[q] = bf16_rne_from_double(tanh(pre + (double)bf16f(E[q])));
+      for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
+      hb[q] = bf16_rne_from_double(tanh(pre + (double)bf16f(E[q])));
+    }
+    *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) =
+        (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
   }
-  *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) =
-      (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+}
+
+// Persistent launch over the active tiles (rows of this step only): the
+// workgroups of XCD x walk the x-th eighth of the tile list. No workgroup is
+// launched just to exit.
+template <bool BF16>
+__global__ __launch_bounds__(RTHREADS) void k_rec(DevState st) {
+  const int R = st.ctrl->R;
+  if (R <= 0) return;
+  const int nra = (R + RT - 1) / RT;
+  const int T = (st.d / RT) * nra;
+  const int x = blockIdx.x & 7, gx = gridDim.x >> 3;
+  const int lo = (int)((long long)T * x / 8), hi = (int)((long long)T * (x + 1) / 8);
+  __shared__ typename std::conditional<BF16, double, float>::type red[RSPLIT][RT * RT];
+  for (int tile = lo + (int)(blockIdx.x >> 3); tile < hi; tile += gx) {
+    const int vt = tile / nra, rt = tile - vt * nra;
+    if constexpr (BF16)
+      rec_tile_bf16(st, red, vt, rt, R);
+    else
+      rec_tile_f32(st, red, vt, rt, R);
+    __syncthreads();   // red is reused by the next tile
+  }
 }
 
 }  // namespace
 
 hipError_t launch_rec(const DevState &st, hipStream_t s) {
-  const int G = xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT));
+  // Multiple of 8; two workgroups per compute unit at most.
+  const int G = std::max(8, std::min(st.n_cu / 4 * 8, xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT))));
   if (st.dtype == 1)
-    hipLaunchKernelGGL(k_rec_bf16, dim3(G), dim3(RTHREADS), 0, s, st);
+    hipLaunchKernelGGL(k_rec<true>, dim3(G), dim3(RTHREADS), 0, s, st);
   else
-    hipLaunchKernelGGL(k_rec_f32, dim3(G), dim3(RTHREADS), 0, s, st);
+    hipLaunchKernelGGL(k_rec<false>, dim3(G), dim3(RTHREADS), 0, s, st);
   return hipGetLastError();
 }
 

@@ -84,6 +84,7 @@ struct DevState {
   int32_t n, k, d, V, M, max_len_cap, refill_thr, S, R_max, dtype, kv_layers, max_inputs;
   int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
+  int32_t n_cu;        // compute units of the device (persistent launches)
   double delta;
   float beta;
 };
