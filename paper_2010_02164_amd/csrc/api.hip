@@ -11,6 +11,7 @@
 
 #include "../../include/streambeam.h"
 #include "sb_internal.h"
+#include "topk.h"
 
 using namespace sb;
 
@@ -45,7 +46,7 @@ namespace {
 constexpr size_t ALIGN = 256;
 
 struct Layout {
-  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, s_status, s_score, s_tok, s_h,
+  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, s_status, s_score, s_tok, s_h,
       s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
       o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, wout_t, total;
 };
@@ -75,6 +76,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.b_steps = take(n * 4);
   L.b_sel = take(n * 4);
   L.b_par = take(n * 4);
+  L.b_ml = take(n * 4);
   L.s_status = take(nk * 4);
   L.s_score = take(nk * 8);
   L.s_tok = take(nk * 4);
@@ -89,7 +91,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.r_Lx = take(Rm * 4);
   L.r_lse = take(Rm * 8);
   L.hbuf = take(Rm * d * es);
-  L.part = take(Rm * S * (2 + 2 * KB) * 4);
+  L.part = take(Rm * S * part_width((int)KB) * 4);
   L.top_lp = take(Rm * k * 8);
   L.top_tok = take(Rm * k * 4);
   L.o_count = take(Q * 4);
@@ -176,7 +178,6 @@ sb_status launch_step(sb_decoder *dec, hipStream_t s, hipEvent_t e0 = nullptr, h
   if (e0) HIPCHK(hipEventRecord(e0, s));
   HIPCHK(launch_proj(st, s));
   if (e1) HIPCHK(hipEventRecord(e1, s));
-  HIPCHK(launch_rowmerge(st, s));
   HIPCHK(launch_beam(st, s));
   if (st.kv_layers > 0) HIPCHK(launch_kv_gather(st, s));
   return SB_OK;
@@ -280,6 +281,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.b_steps = reinterpret_cast<int32_t *>(w + L.b_steps);
   st.b_sel = reinterpret_cast<int32_t *>(w + L.b_sel);
   st.b_par = reinterpret_cast<int32_t *>(w + L.b_par);
+  st.b_ml = reinterpret_cast<int32_t *>(w + L.b_ml);
   st.s_status = reinterpret_cast<int32_t *>(w + L.s_status);
   st.s_score = reinterpret_cast<double *>(w + L.s_score);
   st.s_tok = reinterpret_cast<int32_t *>(w + L.s_tok);

@@ -1,10 +1,10 @@
 // Row merge, per-beam top-k with pruning and finalization, and the
 // backtrack of finished hypotheses.
 //
-//   K_rowmerge : per expanded row, merge the projection's per-tile partials
-//                into log-sum-exp and the row's best k tokens; their
-//                log-probabilities lp = z - lse (Sec. 2 log-likelihoods).
-//   K_beam     : per selected beam, rank the k|V| expansions (only each
+//   K_beam     : per selected beam, merge the projection's per-tile partials
+//                of each active parent's row into its log-sum-exp and best k
+//                tokens, with log-probabilities lp = z - lse (Sec. 2
+//                log-likelihoods); rank the k|V| expansions (only each
 //                parent's best k can reach the top k) plus one no-op per
 //                terminated candidate, keep the top k (Sec. 2), apply the
 //                heuristics H (Sec. 4: relative threshold delta against the
@@ -22,190 +22,285 @@
 namespace sb {
 namespace {
 
+// Wave-wide maximum of a 64-bit key.
+__device__ __forceinline__ cand_key wave_max_key(cand_key x) {
+#pragma unroll
+  for (int mask = 1; mask < 64; mask <<= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)x, mask, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), mask, 64);
+    const cand_key y = ((cand_key)hi << 32) | lo;
+    x = y > x ? y : x;
+  }
+  return x;
+}
+
+// Merge the per-tile partials of one row (one wave). Each lane folds the
+// tiles lane, lane+64, ... into (max, sum exp) and a sorted best-KB list
+// (loads issued a batch at a time before they are folded). The row's
+// log-sum-exp is combined over the lanes and taken from lane 0; the row's k
+// best keys are drawn in k rounds of a wave maximum over the lists' heads,
+// the lane holding the winner dropping it (keys are distinct: they carry
+// the token). Lane r < k receives the key of rank r.
+template <int KB>
+__device__ __forceinline__ double merge_row(const DevState &st, int row, int lane, int k, cand_key &mine) {
+  constexpr int PW = part_width(KB);
+  constexpr int NBT = KB <= 8 ? 4 : 2;   // partials in flight per lane
+  const float *base = st.part + (size_t)row * st.S * PW;
+  float m = -INFINITY, s = 0.0f;
+  TopK<KB> tk;
+  topk_init(tk);
+#pragma unroll 1
+  for (int t0 = lane; t0 < st.S; t0 += 64 * NBT) {
+    float rec[NBT][PW];
+#pragma unroll
+    for (int u = 0; u < NBT; ++u) {
+      const int t = min(t0 + 64 * u, st.S - 1);
+      const uint4 *p = reinterpret_cast<const uint4 *>(base + (size_t)t * PW);
+#pragma unroll
+      for (int x = 0; x < PW / 4; ++x) {
+        const uint4 v = p[x];
+        rec[u][4 * x] = __uint_as_float(v.x);
+        rec[u][4 * x + 1] = __uint_as_float(v.y);
+        rec[u][4 * x + 2] = __uint_as_float(v.z);
+        rec[u][4 * x + 3] = __uint_as_float(v.w);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NBT; ++u) {
+      if (t0 + 64 * u < st.S) {
+        TopK<KB> o;
+        topk_load(o, rec[u] + 2);
+        lse_merge(m, s, rec[u][0], rec[u][1]);
+        topk_merge(tk, o);
+      }
+    }
+  }
+#pragma unroll
+  for (int mask = 1; mask < 64; mask <<= 1) {
+    const float m2 = __shfl_xor(m, mask, 64), s2 = __shfl_xor(s, mask, 64);
+    lse_merge(m, s, m2, s2);
+  }
+  m = __shfl(m, 0, 64);
+  s = __shfl(s, 0, 64);
+  mine = 0ull;
+#pragma unroll 1
+  for (int r = 0; r < k; ++r) {
+    const cand_key best = wave_max_key(tk.k[0]);
+    if (lane == r) mine = best;
+    if (tk.k[0] == best) {
+#pragma unroll
+      for (int j = 0; j + 1 < KB; ++j) tk.k[j] = tk.k[j + 1];
+      tk.k[KB - 1] = 0ull;
+    }
+  }
+  return (double)m + log((double)s);
+}
+
+// Row merge as its own kernel (wave per row), for the single-expansion
+// debug entry point: writes lse and the k best log-probabilities/tokens.
 template <int KB>
 __global__ __launch_bounds__(256) void k_rowmerge(DevState st) {
   const int R = st.ctrl->R;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= R) return;
-  constexpr int PW = 2 + 2 * KB;
-  const float *base = st.part + (size_t)row * st.S * PW;
-  float m = -INFINITY, s = 0.0f;
-  TopK<KB> tk;
-  topk_init(tk);
-#pragma unroll 1
-  for (int t = lane; t < st.S; t += 64) {
-    const float *p = base + (size_t)t * PW;
-    TopK<KB> o;
-    topk_load(o, p + 2);
-    lse_merge(m, s, p[0], p[1]);
-    topk_merge(tk, o);
-  }
-#pragma unroll 1
-  for (int mask = 1; mask < 64; mask <<= 1) {
-    TopK<KB> o;
-    topk_shfl_xor(o, tk, mask);
-    const float m2 = __shfl_xor(m, mask, 64), s2 = __shfl_xor(s, mask, 64);
-    lse_merge(m, s, m2, s2);
-    topk_merge(tk, o);
-  }
-  const double lse = (double)m + log((double)s);
-  if (lane == 0) st.r_lse[row] = lse;
+  cand_key mine;
   const int k = st.k;
-#pragma unroll
-  for (int q = 0; q < KB; ++q) {
-    if (lane == q && q < k) {
-      st.top_lp[(size_t)row * k + q] = (double)key_val(tk.k[q]) - lse;
-      st.top_tok[(size_t)row * k + q] = key_idx(tk.k[q]);
-    }
+  const double lse = merge_row<KB>(st, row, lane, k, mine);
+  if (lane == 0) st.r_lse[row] = lse;
+  if (lane < k) {
+    st.top_lp[(size_t)row * k + lane] = (double)key_val(mine) - lse;
+    st.top_tok[(size_t)row * k + lane] = key_idx(mine);
   }
 }
 
-constexpr int MAXC = KMAX_SUPPORTED * KMAX_SUPPORTED + KMAX_SUPPORTED;
-
-// Ranking key of an expansion: higher score first, then lower parent rank,
-// then lower token (a no-op has token -1).
-__device__ __forceinline__ bool cand_beats(double sa, int pa, int ta, double sb, int pb, int tb) {
-  if (sa != sb) return sa > sb;
-  if (pa != pb) return pa < pb;
-  return ta < tb;
+// Ranking of an expansion: higher score first, then the smaller secondary
+// key (parent rank << 24 | token + 1; a no-op has token -1).
+__device__ __forceinline__ bool ranks_above(double sa, int ka, double sb, int kb) {
+  return sa > sb || (sa == sb && ka < kb);
 }
 
-constexpr int BEAM_THREADS = 256;
+constexpr int BEAM_THREADS = 512;
+constexpr int BEAM_WAVES = BEAM_THREADS / 64;
+constexpr int NO_KEY = 0x7FFFFFFF;
 
+template <int KB>
 __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;   // 0..255
-  // b_sel is cleared for every beam when nothing is live (R == 0).
-  if (!st.b_sel[b]) return;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
   const int k = st.k;
   const int base = b * k;
-  __shared__ double cs[MAXC];
-  __shared__ int cp[MAXC], ct[MAXC], cv[MAXC];
-  __shared__ int at_rank[KMAX_SUPPORTED];
-  __shared__ double nscore[KMAX_SUPPORTED];
-  __shared__ int npar[KMAX_SUPPORTED], ntok[KMAX_SUPPORTED], nstat[KMAX_SUPPORTED];
-  __shared__ int kept_per[KMAX_SUPPORTED];
-  __shared__ int nw_sh, nact_sh, nvalid_sh;
-  // The beam's slots, read once (one parallel round of loads).
+  // Everything the beam needs from its records is loaded in one round,
+  // before the selection flag is tested.
+  int my_status = SLOT_EMPTY, my_row = -1;
+  double my_score = 0.0;
+  if (tid < k) {
+    my_status = st.s_status[base + tid];
+    my_row = st.s_row[base + tid];
+    my_score = st.s_score[base + tid];
+  }
+  int my_q = 0, my_t = 0, my_ml = 0;
+  if (tid == 64) {
+    my_q = st.b_input[b];
+    my_t = st.b_steps[b] + 1;     // 1-based index of the emitted token
+    my_ml = st.b_ml[b];
+  }
+  // b_sel is cleared for every beam when nothing is live (R == 0).
+  if (!st.b_sel[b]) return;
   __shared__ int sl_status[KMAX_SUPPORTED], sl_row[KMAX_SUPPORTED];
   __shared__ double sl_score[KMAX_SUPPORTED];
   __shared__ int q_in_sh, t_sh, max_len_sh;
-
-  if (lane < k) {
-    sl_status[lane] = st.s_status[base + lane];
-    sl_row[lane] = st.s_row[base + lane];
-    sl_score[lane] = st.s_score[base + lane];
+  // Best k log-probabilities and tokens of each active parent's row.
+  __shared__ double ch_lp[KMAX_SUPPORTED * KMAX_SUPPORTED];
+  __shared__ int ch_tok[KMAX_SUPPORTED * KMAX_SUPPORTED];
+  // The pruned new beam, in rank order.
+  __shared__ double nscore[KMAX_SUPPORTED];
+  __shared__ int npar[KMAX_SUPPORTED], ntok[KMAX_SUPPORTED], nstat[KMAX_SUPPORTED];
+  __shared__ int nw_sh, nact_sh;
+  if (tid < k) {
+    sl_status[tid] = my_status;
+    sl_row[tid] = my_row;
+    sl_score[tid] = my_score;
   }
-  if (lane == 64) {
-    const int q = st.b_input[b];
-    q_in_sh = q;
-    t_sh = st.b_steps[b] + 1;     // 1-based index of the emitted token
-    max_len_sh = st.q_ml[q];
+  if (tid == 64) {
+    q_in_sh = my_q;
+    t_sh = my_t;
+    max_len_sh = my_ml;
   }
-  if (lane == 128) nvalid_sh = 0;
-  if (lane >= 192 && lane < 192 + KMAX_SUPPORTED) at_rank[lane - 192] = -1;
   __syncthreads();
   const int q_in = q_in_sh, t = t_sh, max_len = max_len_sh;
 
-  // Candidate set: child c of parent j at index j*k + c; no-op of parent j
-  // at index k*k + j.
-  const int C = k * k + k;
-  for (int q = lane; q < C; q += BEAM_THREADS) {
-    int valid = 0, par, tok = -1;
-    double sc = 0.0;
-    if (q < k * k) {
-      par = q / k;
-      const int c = q - par * k;
-      if (sl_status[par] == SLOT_ACTIVE) {
-        const int r = sl_row[par];
-        sc = sl_score[par] + st.top_lp[(size_t)r * k + c];
-        tok = st.top_tok[(size_t)r * k + c];
-        valid = tok >= 0 && tok < st.V;
-      }
-    } else {
-      par = q - k * k;
-      const int status = sl_status[par];
-      if (status == SLOT_EOS || status == SLOT_MAXLEN) {
-        sc = sl_score[par];
-        valid = 1;
-      }
+  // Row merge of every active parent: wave w takes parents w, w+8.
+  for (int par = wave; par < k; par += BEAM_WAVES) {
+    if (sl_status[par] != SLOT_ACTIVE) continue;
+    cand_key mine;
+    const double lse = merge_row<KB>(st, sl_row[par], lane, k, mine);
+    if (lane < k) {
+      ch_lp[par * k + lane] = (double)key_val(mine) - lse;
+      ch_tok[par * k + lane] = key_idx(mine);
     }
-    cs[q] = sc;
-    cp[q] = par;
-    ct[q] = tok;
-    cv[q] = valid;
-    if (valid) atomicAdd(&nvalid_sh, 1);
   }
   __syncthreads();
 
-  // Full beam B': rank of every valid candidate among the valid ones.
-  for (int q = lane; q < C; q += BEAM_THREADS) {
-    if (!cv[q]) continue;
-    int rank = 0;
-    for (int o = 0; o < C; ++o)
-      rank += (cv[o] && cand_beats(cs[o], cp[o], ct[o], cs[q], cp[q], ct[q]));
-    if (rank < k) at_rank[rank] = q;
-  }
-  __syncthreads();
-
-  // Heuristics H and termination, in rank order (at most k entries).
-  if (lane == 0) {
-    const int full = min(k, nvalid_sh);
-    const double ref = at_rank[0] >= 0 ? cs[at_rank[0]] : 0.0;
-    for (int j = 0; j < k; ++j) kept_per[j] = 0;
-    int w = 0, nact = 0;
-    for (int r = 0; r < full; ++r) {
-      const int q = at_rank[r];
-      if (q < 0) break;
-      const double sc = cs[q];
-      const int par = cp[q], tok = ct[q];
-      if (sc < ref - st.delta) continue;            // relative threshold
-      int status;
-      if (tok < 0) {
-        status = sl_status[par];                   // no-op keeps EOS / MAXLEN
-      } else {
-        if (kept_per[par] >= st.M) continue;       // max candidates per parent
-        kept_per[par] += 1;
-        status = tok == 0 ? SLOT_EOS : (t == max_len ? SLOT_MAXLEN : SLOT_ACTIVE);
+  if (wave == 0) {
+    // Full beam B' (Sec. 2): the best k of the k|V| expansions plus one
+    // no-op per terminated candidate. Each parent's expansions arrive
+    // sorted, so B' is a k-way merge: lane p < k holds the head of parent
+    // p's list, lane k + p the no-op of parent p; each round takes the
+    // best head (wave maximum) and its lane advances.
+    const bool is_list = lane < k, is_noop = lane >= k && lane < 2 * k;
+    const int p = is_list ? lane : lane - k;
+    const int pstat = (is_list || is_noop) ? sl_status[p] : SLOT_EMPTY;
+    int hp = 0;
+    bool noop_left = is_noop && (pstat == SLOT_EOS || pstat == SLOT_MAXLEN);
+    double hs = -INFINITY;
+    int hk = NO_KEY;
+    auto head = [&]() {
+      hs = -INFINITY;
+      hk = NO_KEY;
+      if (is_list && pstat == SLOT_ACTIVE && hp < k) {
+        const int tok = ch_tok[p * k + hp];
+        if (tok >= 0 && tok < st.V) {
+          hs = sl_score[p] + ch_lp[p * k + hp];
+          hk = (p << 24) | (tok + 1);
+        }
+      } else if (noop_left) {
+        hs = sl_score[p];
+        hk = p << 24;
       }
-      nscore[w] = sc;
-      npar[w] = par;
-      ntok[w] = tok;
-      nstat[w] = status;
-      nact += status == SLOT_ACTIVE;
-      ++w;
+    };
+    head();
+    double rs = -INFINITY;   // lane r: the entry of rank r
+    int rk = NO_KEY;
+    int nfull = 0;
+#pragma unroll 1
+    for (int r = 0; r < k; ++r) {
+      double bs = hs;
+      int bk = hk;
+#pragma unroll
+      for (int mask = 1; mask < 64; mask <<= 1) {
+        const double os = __shfl_xor(bs, mask, 64);
+        const int ok = __shfl_xor(bk, mask, 64);
+        if (ranks_above(os, ok, bs, bk)) {
+          bs = os;
+          bk = ok;
+        }
+      }
+      if (bk == NO_KEY) break;   // fewer than k candidates
+      if (lane == r) {
+        rs = bs;
+        rk = bk;
+      }
+      nfull = r + 1;
+      if (hk == bk) {            // the winner's lane advances
+        if (is_list) ++hp;
+        else noop_left = false;
+        head();
+      }
     }
-    nw_sh = w;
-    nact_sh = nact;
+    // Heuristics H (Sec. 4) on B' in rank order: drop x if
+    // score(x) < best - delta, best = B'[0] (possibly terminated, App. A.3);
+    // drop an expansion whose parent already has M kept expansions (no-ops
+    // exempt). A parent's kept expansions before rank r are its first M
+    // delta-survivors, so the M test needs only their count.
+    const double ref = __shfl(rs, 0, 64);
+    const int rpar = rk >> 24, rtok = (rk & 0xFFFFFF) - 1;
+    const bool keepd = lane < nfull && !(rs < ref - st.delta);
+    int before = 0;
+#pragma unroll 1
+    for (int o = 0; o < nfull; ++o) {
+      const int okk = __shfl(rk, o, 64);
+      const int okeep = __shfl((int)keepd, o, 64);
+      before += (o < lane && okeep && (okk >> 24) == rpar && (okk & 0xFFFFFF) != 0);
+    }
+    const bool kept = keepd && (rtok < 0 || before < st.M);
+    int status = SLOT_EMPTY;
+    if (kept) {
+      if (rtok < 0) status = sl_status[rpar];                   // no-op keeps EOS / MAXLEN
+      else status = rtok == 0 ? SLOT_EOS : (t == max_len ? SLOT_MAXLEN : SLOT_ACTIVE);
+    }
+    const unsigned long long km = __ballot(kept);
+    const unsigned long long am = __ballot(kept && status == SLOT_ACTIVE);
+    if (kept) {
+      const int nr = __popcll(km & ((1ull << lane) - 1ull));
+      nscore[nr] = rs;
+      npar[nr] = rpar;
+      ntok[nr] = rtok;
+      nstat[nr] = status;
+    }
+    if (lane == 0) {
+      nw_sh = __popcll(km);
+      nact_sh = __popcll(am);
+    }
   }
   __syncthreads();
   const int w = nw_sh;
   const bool ends = nact_sh == 0;
 
   // History: backpointers of level t, indexed by the input's queue position.
-  if (lane < w) {
-    const uint32_t tokbits = ntok[lane] < 0 ? BP_NOOP : (uint32_t)ntok[lane];
-    st.bp[((size_t)q_in * st.max_len_cap + (t - 1)) * k + lane] = ((uint32_t)npar[lane] << 24) | tokbits;
+  if (tid < w) {
+    const uint32_t tokbits = ntok[tid] < 0 ? BP_NOOP : (uint32_t)ntok[tid];
+    st.bp[((size_t)q_in * st.max_len_cap + (t - 1)) * k + tid] = ((uint32_t)npar[tid] << 24) | tokbits;
   }
 
   if (ends) {
     // Y[i] = the survivors in rank order; tokens are rebuilt later.
     const int fin = (int)st.ctrl->timesteps;
-    if (lane < w) {
+    if (tid < w) {
       OutHyp h;
-      h.score = nscore[lane];
+      h.score = nscore[tid];
       h.length = 0;
-      h.status = nstat[lane];
+      h.status = nstat[tid];
       h.finalize_step = fin;
       h.level = t;
-      st.o_hyp[(size_t)q_in * k + lane] = h;
+      st.o_hyp[(size_t)q_in * k + tid] = h;
     }
-    if (lane < k) {
-      st.s_status[base + lane] = SLOT_EMPTY;
-      st.s_prow[base + lane] = -1;
+    if (tid < k) {
+      st.s_status[base + tid] = SLOT_EMPTY;
+      st.s_prow[base + tid] = -1;
     }
-    if (lane == 0) {
+    if (tid == 0) {
       st.o_count[q_in] = w;
       st.b_input[b] = -1;
       atomicAdd(reinterpret_cast<unsigned long long *>(&st.ctrl->hyps), (unsigned long long)w);
@@ -216,19 +311,19 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
 
   // Continue: write the new beam into ranks 0..w-1 (no-ops keep their
   // state; active children take their parent's new state h).
-  if (lane < k) {
-    if (lane < w) {
-      const int par = npar[lane];
-      st.s_status[base + lane] = nstat[lane];
-      st.s_score[base + lane] = nscore[lane];
-      if (ntok[lane] >= 0) st.s_tok[base + lane] = ntok[lane];
-      st.s_prow[base + lane] = nstat[lane] == SLOT_ACTIVE ? sl_row[par] : -1;
+  if (tid < k) {
+    if (tid < w) {
+      const int par = npar[tid];
+      st.s_status[base + tid] = nstat[tid];
+      st.s_score[base + tid] = nscore[tid];
+      if (ntok[tid] >= 0) st.s_tok[base + tid] = ntok[tid];
+      st.s_prow[base + tid] = nstat[tid] == SLOT_ACTIVE ? sl_row[par] : -1;
     } else {
-      st.s_status[base + lane] = SLOT_EMPTY;
-      st.s_prow[base + lane] = -1;
+      st.s_status[base + tid] = SLOT_EMPTY;
+      st.s_prow[base + tid] = -1;
     }
   }
-  if (lane == 0) {
+  if (tid == 0) {
     st.b_steps[b] = t;
     st.b_par[b] ^= 1;
   }
@@ -236,25 +331,12 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   // flattened over (survivor, 16-byte chunk) so all threads stream.
   const int rowbytes = st.d * (st.dtype == 1 ? 2 : 4);
   const int chunks = rowbytes / 16;
-  __shared__ int cp_src[KMAX_SUPPORTED], cp_dst[KMAX_SUPPORTED];
-  __shared__ int ncopy;
-  if (lane == 0) {
-    int c = 0;
-    for (int r = 0; r < w; ++r)
-      if (nstat[r] == SLOT_ACTIVE) {
-        cp_src[c] = sl_row[npar[r]];
-        cp_dst[c] = base + r;
-        ++c;
-      }
-    ncopy = c;
-  }
-  __syncthreads();
   const uint4 *__restrict__ hb = static_cast<const uint4 *>(st.hbuf);
   uint4 *__restrict__ sh = static_cast<uint4 *>(st.s_h);
-  const int total = ncopy * chunks;
-  for (int x = lane; x < total; x += BEAM_THREADS) {
+  const int total = w * chunks;
+  for (int x = tid; x < total; x += BEAM_THREADS) {
     const int r = x / chunks, c = x - r * chunks;
-    sh[(size_t)cp_dst[r] * chunks + c] = hb[(size_t)cp_src[r] * chunks + c];
+    if (nstat[r] == SLOT_ACTIVE) sh[(size_t)(base + r) * chunks + c] = hb[(size_t)sl_row[npar[r]] * chunks + c];
   }
 }
 
@@ -301,7 +383,11 @@ hipError_t launch_rowmerge(const DevState &st, hipStream_t s) {
 }
 
 hipError_t launch_beam(const DevState &st, hipStream_t s) {
-  hipLaunchKernelGGL(k_beam, dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+  switch (st.kbucket) {
+    case 4: hipLaunchKernelGGL((k_beam<4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
+    case 8: hipLaunchKernelGGL((k_beam<8>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
+    default: hipLaunchKernelGGL((k_beam<16>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
+  }
   return hipGetLastError();
 }
 

@@ -38,7 +38,7 @@ template <int KB>
 union ProjSmem {
   unsigned char B[2][2][TR][LS];          // [buffer][K half][row][byte]
   float red[2][4][2][16][64];             // [sending half][slice][block][reg][lane]
-  float xch[4][TR][2 + 2 * KB];           // [slice][row][max, sumexp, keys]
+  float xch[4][TR][part_width(KB)];       // [slice][row][max, sumexp, keys]
 };
 
 // K loop of one wave over its half: acc[b] (b < NBV) += W_out fragment x
@@ -192,7 +192,7 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
   // Epilogue on the owned blocks. Block 2g+bl: lane holds batch row
   // r0 + 32(2g+bl) + l32 and the wave's vocabulary rows
   // v0 + 32wv + 8*(reg/4) + 4h + reg%4, increasing with reg.
-  constexpr int PW = 2 + 2 * KB;
+  constexpr int PW = part_width(KB);
   TopK<KB> tks[2];
   float ms[2], ss[2];
 #pragma unroll
@@ -262,10 +262,17 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
         lse_merge(m, s, p[0], p[1]);
         topk_merge(tk, o);
       }
-      float *out = st.part + ((size_t)j * st.S + vt) * PW;
-      out[0] = m;
-      out[1] = s;
-      topk_store(out + 2, tk);
+      float rec[PW];
+      rec[0] = m;
+      rec[1] = s;
+      topk_store(rec + 2, tk);
+#pragma unroll
+      for (int x = 2 + 2 * KB; x < PW; ++x) rec[x] = 0.0f;
+      u4 *out = reinterpret_cast<u4 *>(st.part + ((size_t)j * st.S + vt) * PW);
+#pragma unroll
+      for (int x = 0; x < PW / 4; ++x)
+        out[x] = u4{__float_as_uint(rec[4 * x]), __float_as_uint(rec[4 * x + 1]), __float_as_uint(rec[4 * x + 2]),
+                    __float_as_uint(rec[4 * x + 3])};
     }
   }
 }

@@ -47,6 +47,7 @@ struct DevState {
   int32_t *b_steps;    // l_t: steps taken
   int32_t *b_sel;      // 1 if expanded this step
   int32_t *b_par;      // which KV buffer holds this beam's state
+  int32_t *b_ml;       // max_len of the beam's input
   // candidate slots [n*k], slot = beam*k + rank
   int32_t *s_status;
   double *s_score;

@@ -130,6 +130,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
           st.b_input[b] = inp[u];
           st.b_steps[b] = 0;
           st.b_par[b] = 0;
+          st.b_ml[b] = st.q_ml[inp[u]];
           for (int j = 0; j < k; ++j) {
             st.s_status[b * k + j] = j == 0 ? SLOT_ACTIVE : SLOT_EMPTY;
             st.s_score[b * k + j] = 0.0;

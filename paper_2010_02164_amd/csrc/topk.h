@@ -103,6 +103,10 @@ __device__ __forceinline__ void topk_load(TopK<K> &t, const float *p) {
     t.k[j] = ((cand_key)__float_as_uint(p[2 * j + 1]) << 32) | __float_as_uint(p[2 * j]);
 }
 
+// Floats per partial record (max, sum exp, kb keys as two words each),
+// padded to a multiple of 4 so that records are 16-byte aligned.
+__host__ __device__ constexpr int part_width(int kb) { return (2 + 2 * kb + 3) & ~3; }
+
 // (m, s) represents log(s) + m: a running max and a sum of exp(z - m).
 __device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2) {
   const float M = fmaxf(m, m2);
