@@ -108,7 +108,7 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--sched", default="var_stream", choices=["fixed", "var_batch", "var_stream"])
+    ap.add_argument("--sched", default="var_stream", choices=["fixed", "var_batch", "var_stream", "var_fifo"])
     ap.add_argument("--eps", type=float, default=None)
     ap.add_argument("--cpu-sample", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -132,7 +132,7 @@ def main():
 
     cfg = get_config(args.config)
     eps = cfg.eps if args.eps is None else args.eps
-    if args.sched != "var_stream":
+    if args.sched not in ("var_stream", "var_fifo"):
         eps = 0.0
     wl = make_workload(cfg)
     weights = weights_to_device(wl)

@@ -50,8 +50,12 @@ typedef enum {
  * paper's own finalization rule (App. A.1: eps = 0, no pruning); Var-Batch =
  * variable-width search, refill only when the batch is empty (eps = 0);
  * Var-Stream = refill when at most eps*n beams remain, expand only the beams
- * with the fewest steps taken. */
-typedef enum { SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2 } sb_sched;
+ * with the fewest steps taken; Var-Str-FIFO (App. A, alternative method
+ * analysis) = Var-Stream's refill, but every live beam is expanded at each
+ * timestep (the batch capacity n taken from the beam with the most steps
+ * down; at most n beams are live). All four return the same outputs for
+ * the same parameters (eps, delta, M as forced below). */
+typedef enum { SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2, SB_VAR_FIFO = 3 } sb_sched;
 
 /* Storage type of weights, h0 and decoder states. SB_F32: fp32 everywhere
  * (MFMA fp32, fp32 accumulation). SB_BF16: bf16 weights and states; the

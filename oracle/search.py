@@ -70,14 +70,20 @@ class _Beam:
 
 def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
            n: int, eps: float, k: int, delta: float = math.inf,
-           M: Optional[int] = None, on_step: Optional[Callable] = None) -> SearchResult:
+           M: Optional[int] = None, on_step: Optional[Callable] = None,
+           select: str = "min_steps") -> SearchResult:
     """Run Alg. 1 over inputs 0..N-1 (h0[i] is e_i = E(x_i)).
 
     `decoder` needs initial_state(h0_row) and expand(h_prev, y, t, Lx) ->
     (h, lp) as in oracle.decoder.ElmanDecoder (tests substitute scripted
     decoders). `on_step(timestep, selected_inputs, rows)` observes the
-    schedule.
+    schedule. `select` is Alg. 1's beam selection, "min_steps" (the beams
+    with minimal l_t), or "fifo" for Var-Str-FIFO (App. A, alternative
+    method analysis: beams up to the batch capacity n, starting from the
+    one with maximal l_t).
     """
+    if select not in ("min_steps", "fifo"):
+        raise ValueError(select)
     N = len(Lx)
     M = k if M is None else int(M)
     if not (k >= 1 and n >= 1 and 0.0 <= eps < 1.0 and 1 <= M <= k):
@@ -98,7 +104,12 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
             res.refills += 1
             res.admitted += m
         lmin = min(b.steps for b in live)
-        sel = [b for b in live if b.steps == lmin]
+        if select == "fifo":
+            # At most n beams are live, so the capacity-n prefix of the
+            # beams ordered by decreasing l_t is every live beam.
+            sel = sorted(live, key=lambda b: -b.steps)[:n]
+        else:
+            sel = [b for b in live if b.steps == lmin]
 
         # One batched decoder call over every active candidate of the
         # selected beams (the inner loops of Alg. 1).
@@ -144,7 +155,8 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
 def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var_stream",
                     inputs: Optional[Sequence[int]] = None, decoder=None) -> SearchResult:
     """Convenience wrapper: decode (a subset of) a synthgen Workload with its
-    config's parameters; `sched` picks Fixed / Var-Batch / Var-Stream."""
+    config's parameters; `sched` picks Fixed / Var-Batch / Var-Stream /
+    Var-Str-FIFO ("var_fifo")."""
     from .decoder import ElmanDecoder
     c = wl.cfg
     dec = decoder or ElmanDecoder.from_workload(wl)
@@ -157,7 +169,8 @@ def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var
         eps, delta, M = 0.0, math.inf, k
     elif sched == "var_batch":
         eps = 0.0
-    elif sched != "var_stream":
+    elif sched not in ("var_stream", "var_fifo"):
         raise ValueError(sched)
     idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
-    return decode(dec, wl.h0[idx], wl.Lx[idx], wl.max_len[idx], n, eps, k, delta, M)
+    return decode(dec, wl.h0[idx], wl.Lx[idx], wl.max_len[idx], n, eps, k, delta, M,
+                  select="fifo" if sched == "var_fifo" else "min_steps")

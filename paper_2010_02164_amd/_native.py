@@ -17,9 +17,10 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "streambeam.h")
 
 SB_OK, SB_E_INVALID_ARG, SB_E_WORKSPACE, SB_E_STATE, SB_E_QUEUE_FULL, SB_E_TRUNCATED, \
     SB_E_HIP, SB_E_UNSUPPORTED = range(8)
-SB_FIXED, SB_VAR_BATCH, SB_VAR_STREAM = 0, 1, 2
+SB_FIXED, SB_VAR_BATCH, SB_VAR_STREAM, SB_VAR_FIFO = 0, 1, 2, 3
 SB_F32, SB_BF16 = 0, 1
-SCHEDULERS = {"fixed": SB_FIXED, "var_batch": SB_VAR_BATCH, "var_stream": SB_VAR_STREAM}
+SCHEDULERS = {"fixed": SB_FIXED, "var_batch": SB_VAR_BATCH, "var_stream": SB_VAR_STREAM,
+              "var_fifo": SB_VAR_FIFO}
 
 
 class SbParams(ctypes.Structure):

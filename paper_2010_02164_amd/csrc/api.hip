@@ -125,7 +125,7 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   if (!(p->eps >= 0.0 && p->eps < 1.0)) return bad(SB_E_INVALID_ARG, "eps must be in [0, 1)");
   if (!(p->delta > 0.0)) return bad(SB_E_INVALID_ARG, "delta must be > 0 (use +inf to disable)");
   if (p->max_per_node < 1 || p->max_per_node > p->k) return bad(SB_E_INVALID_ARG, "max_per_node must be in [1, k]");
-  if (p->sched < SB_FIXED || p->sched > SB_VAR_STREAM) return bad(SB_E_INVALID_ARG, "unknown scheduler");
+  if (p->sched < SB_FIXED || p->sched > SB_VAR_FIFO) return bad(SB_E_INVALID_ARG, "unknown scheduler");
   if (p->max_len_cap < 1 || p->max_len_cap > 4096) return bad(SB_E_INVALID_ARG, "max_len_cap must be in [1, 4096]");
   if (p->max_inputs < 1) return bad(SB_E_INVALID_ARG, "max_inputs must be >= 1");
   const int64_t es = m->dtype == SB_BF16 ? 2 : 4;
@@ -327,6 +327,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.max_inputs = p.max_inputs;
   st.kbucket = kbucket_of(p.k);
   st.hist_width = std::max(16, (st.R_max + 63) / 64);
+  st.select_all = p.sched == SB_VAR_FIFO ? 1 : 0;
   {
     int dev = 0, ncu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||

@@ -19,7 +19,7 @@ struct DevCtrl {
   int32_t n_queued;   // inputs submitted so far
   int32_t cursor;     // next input to admit (Alg. 1's c)
   int32_t R;          // rows (active candidates) expanded this step
-  int32_t t_sel;      // 1-based index of the token the selected beams emit
+  int32_t t_sel;      // smallest 1-based output position among the selected beams
   int32_t live;       // live beams after admission
   int32_t done;       // 1: nothing queued and no beam live
   int32_t n_sel;      // beams selected this step
@@ -86,6 +86,7 @@ struct DevState {
   int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   int32_t n_cu;        // compute units of the device (persistent launches)
+  int32_t select_all;  // 1: expand every live beam (Var-Str-FIFO), 0: minimal l_t only
   double delta;
   float beta;
 };

@@ -142,7 +142,9 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     }
   }
 
-  // Selection: the live beams with the fewest steps taken.
+  // Selection: the live beams with the fewest steps taken, or every live
+  // beam (Var-Str-FIFO: the capacity n, from the beam with the most steps
+  // down, covers all of them).
   int mn_l = INT_MAX;
 #pragma unroll
   for (int u = 0; u < SCHED_MAXB; ++u)
@@ -156,7 +158,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
 #pragma unroll
   for (int u = 0; u < SCHED_MAXB; ++u) {
     amask[u] = 0u;
-    const bool sel = u < nb && inp[u] >= 0 && stp[u] == mn;
+    const bool sel = u < nb && inp[u] >= 0 && (st.select_all || stp[u] == mn);
     sel_l += sel;
     if (sel) {
       for (int j = 0; j < k; ++j) {
@@ -176,16 +178,16 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
   for (int u = 0; u < SCHED_MAXB; ++u) {
     if (u < nb) {
       const int b = b0 + u;
-      const bool sel = inp[u] >= 0 && stp[u] == mn;
+      const bool sel = inp[u] >= 0 && (st.select_all || stp[u] == mn);
       st.b_sel[b] = sel;
       const int lx = sel ? st.q_Lx[inp[u]] : 0;
       for (int j = 0; j < k; ++j) {
         const int s = b * k + j;
         if ((amask[u] >> j) & 1u) {
           st.r_slot[row] = s;
-          st.r_hsrc[row] = mn == 0 ? -1 - inp[u] : s;   // a fresh beam reads its encoding h0
+          st.r_hsrc[row] = stp[u] == 0 ? -1 - inp[u] : s;   // a fresh beam reads its encoding h0
           st.r_y[row] = st.s_tok[s];
-          st.r_t[row] = mn + 1;
+          st.r_t[row] = stp[u] + 1;
           st.r_Lx[row] = lx;
           st.s_row[s] = row;
           ++row;

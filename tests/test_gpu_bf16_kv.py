@@ -13,7 +13,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("sched,eps", [("var_batch", None), ("var_stream", 0.125), ("var_stream", 0.5),
-                                       ("fixed", None)])
+                                       ("fixed", None), ("var_fifo", 0.25)])
 def test_cfg4_reduced(gpu, sched, eps):
     wl = make_workload(scaled(4, N=48, n=16, V=8000))
     rep, _, _, _ = check_parity(wl, sched, eps=eps)
@@ -21,9 +21,10 @@ def test_cfg4_reduced(gpu, sched, eps):
     assert rep.max_score_err < 1e-4
 
 
-def test_cfg5_reduced_search(gpu):
+@pytest.mark.parametrize("sched", ["var_stream", "var_fifo"])
+def test_cfg5_reduced_search(gpu, sched):
     wl = make_workload(scaled(5, N=24, n=8, V=6000, len_hi=30))
-    check_parity(wl, "var_stream")
+    check_parity(wl, sched)
 
 
 def _kv_reference(wl, dec_o, i, tokens):
@@ -39,14 +40,17 @@ def _kv_reference(wl, dec_o, i, tokens):
     return np.stack(rows, axis=2)   # [L, 2, t, d]
 
 
-def test_cfg5_kv_rows(gpu):
+@pytest.mark.parametrize("sched", ["var_stream", "var_fifo"])
+def test_cfg5_kv_rows(gpu, sched):
     import torch
     from paper_2010_02164_amd import decoder_for_workload, inputs_to_device
-    wl = make_workload(scaled(5, N=6, n=6, V=6000, len_hi=40))
+    # n below N: refills put beams at different steps side by side (under
+    # Var-Str-FIFO they are expanded in the same timestep).
+    wl = make_workload(scaled(5, N=9, n=6, V=6000, len_hi=40))
     c = wl.cfg
-    dec = decoder_for_workload(wl, sched="var_stream")
+    dec = decoder_for_workload(wl, sched=sched, eps=0.5)
     dec.submit(inputs_to_device(wl), wl.Lx, wl.max_len)
-    for _ in range(5):
+    for _ in range(12):
         dec.step(sync=True)
     o = ElmanDecoder.from_workload(wl)
     checked, diff_ulps = 0, []

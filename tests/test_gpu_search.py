@@ -1,5 +1,5 @@
 """End-to-end parity of the HIP search with the oracle (Fixed, Var-Batch,
-Var-Stream), batch invariance and determinism."""
+Var-Stream, Var-Str-FIFO), batch invariance and determinism."""
 import numpy as np
 import pytest
 
@@ -8,7 +8,7 @@ from tests.gpu_util import check_parity, gpu_decode
 
 pytestmark = pytest.mark.gpu
 
-SCHEDS = ["fixed", "var_batch", "var_stream"]
+SCHEDS = ["fixed", "var_batch", "var_stream", "var_fifo"]
 
 
 @pytest.mark.parametrize("sched", SCHEDS)
@@ -23,7 +23,7 @@ def test_cfg2_reduced(gpu, sched):
     check_parity(wl, sched)
 
 
-@pytest.mark.parametrize("sched", ["var_batch", "var_stream"])
+@pytest.mark.parametrize("sched", ["var_batch", "var_stream", "var_fifo"])
 def test_cfg3_reduced(gpu, sched):
     wl = make_workload(scaled(3, N=40, n=16, V=8000))
     check_parity(wl, sched)
@@ -37,10 +37,13 @@ def test_stream_equals_batch_on_gpu_bitwise(gpu):
     a, sa, _ = gpu_decode(wl, "var_batch")
     b, sb, _ = gpu_decode(wl, "var_stream")
     c, _, _ = gpu_decode(wl, "var_stream", eps=0.5, n=5)
-    for ya, yb, yc in zip(a, b, c):
-        assert [(h.tokens, h.score, h.status) for h in ya] == [(h.tokens, h.score, h.status) for h in yb]
-        assert [(h.tokens, h.score, h.status) for h in ya] == [(h.tokens, h.score, h.status) for h in yc]
-    assert sa["expansions"] == sb["expansions"]
+    f, sf, _ = gpu_decode(wl, "var_fifo", eps=0.5, n=6)
+    for ya, yb, yc, yf in zip(a, b, c, f):
+        key = [(h.tokens, h.score, h.status) for h in ya]
+        assert key == [(h.tokens, h.score, h.status) for h in yb]
+        assert key == [(h.tokens, h.score, h.status) for h in yc]
+        assert key == [(h.tokens, h.score, h.status) for h in yf]
+    assert sa["expansions"] == sb["expansions"] == sf["expansions"]
 
 
 def test_deterministic(gpu):

@@ -127,6 +127,24 @@ def test_var_stream_matches_var_batch(cfg_seed, n, eps):
     assert max(vs.rows_per_step) <= n * cfg.k and max(vb.rows_per_step) <= n * cfg.k
 
 
+@pytest.mark.parametrize("cfg_seed,n,eps", [(0, 4, 0.25), (2, 3, 1 / 3), (3, 8, 0.5)])
+def test_var_fifo_matches_var_batch(cfg_seed, n, eps):
+    # App. A (alternative method analysis, Table 4): Var-Str-FIFO changes only
+    # which beams are expanded at a timestep, so outputs and the number of
+    # expanded candidates equal Var-Batch's.
+    cfg = scaled(1, N=21, V=60, d=12, len_hi=9, seed=7000 + cfg_seed, delta=1.2, M=3, k=4)
+    wl = make_workload(cfg)
+    vb = decode_workload(wl, n=n, sched="var_batch")
+    vf = decode_workload(wl, n=n, eps=eps, sched="var_fifo")
+    _same_outputs(vb, vf)
+    assert vb.expansions == vf.expansions and vb.noops == vf.noops
+    assert max(vf.rows_per_step) <= n * cfg.k
+    # Refilling only an empty batch keeps every live beam at the same l_t:
+    # with eps = 0 the FIFO selection is Var-Batch's schedule step for step.
+    v0 = decode_workload(wl, n=n, eps=0.0, sched="var_fifo")
+    assert v0.rows_per_step == vb.rows_per_step and list(v0.finalize_step) == list(vb.finalize_step)
+
+
 def test_fixed_stream_matches_fixed():
     # App. A.1 / Table 3: streaming applied to fixed width (eps > 0) returns
     # what Fixed-Ours (eps = 0) returns.
@@ -138,9 +156,10 @@ def test_fixed_stream_matches_fixed():
     assert a.expansions == b.expansions
 
 
-def _replay(widths, n, eps):
+def _replay(widths, n, eps, fifo=False):
     """Independent event simulation of Alg. 1's schedule from each input's
-    per-step active widths: returns (rows per timestep, finalize timesteps)."""
+    per-step active widths: returns (rows per timestep, finalize timesteps).
+    fifo: every live beam steps (Var-Str-FIFO); else the minimal-l_t ones."""
     N = len(widths)
     c, live, rows, fin = 0, [], [], [0] * N
     while c < N or live:
@@ -149,7 +168,7 @@ def _replay(widths, n, eps):
             live += [[i, 0] for i in range(c, c + m)]
             c += m
         lo = min(s for _, s in live)
-        sel = [b for b in live if b[1] == lo]
+        sel = list(live) if fifo else [b for b in live if b[1] == lo]
         rows.append(sum(widths[i][s] for i, s in sel))
         for b in sel:
             b[1] += 1
@@ -168,6 +187,15 @@ def test_schedule_event_replay(eps):
     assert fin == list(res.finalize_step)
 
 
+@pytest.mark.parametrize("eps", [0.25, 0.5])
+def test_fifo_schedule_event_replay(eps):
+    wl = make_workload(scaled(1, N=30, V=50, d=12, len_hi=12))
+    res = decode_workload(wl, n=6, eps=eps, sched="var_fifo")
+    rows, fin = _replay(res.widths, 6, eps, fifo=True)
+    assert rows == res.rows_per_step
+    assert fin == list(res.finalize_step)
+
+
 def test_fig1_schedule():
     with open(os.path.join(GOLDEN, "fig1_schedule.json")) as f:
         g = json.load(f)
@@ -182,3 +210,10 @@ def test_fig1_schedule():
     assert vb.timesteps == g["var_batch_timesteps"]
     assert list(vb.finalize_step) == g["var_batch_finalize_step"]
     assert vb.expansions == res.expansions
+    trace = []
+    vf = decode(LengthDecoder(g["V"]), np.zeros((len(L), 1)), L, [50] * len(L), n=g["n"],
+                eps=g["eps"], k=g["k"], on_step=lambda t, sel, r: trace.append([t, sorted(sel)]),
+                select="fifo")
+    assert trace == g["var_fifo_trace"]
+    assert list(vf.finalize_step) == g["var_fifo_finalize_step"]
+    assert vf.expansions == res.expansions
