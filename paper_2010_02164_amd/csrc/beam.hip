@@ -18,20 +18,47 @@
 //                backpointer history, one thread per hypothesis.
 #include "sb_internal.h"
 #include "topk.h"
+#include "wave.h"
 
 namespace sb {
 namespace {
 
-// Wave-wide maximum of a 64-bit key.
+// Wave-wide maximum of a 64-bit key, in every lane.
+template <int S>
+__device__ __forceinline__ cand_key max_stage(cand_key x) {
+  cand_key a, b;
+  stage64<S>(x, a, b);
+  return a > b ? a : b;
+}
 __device__ __forceinline__ cand_key wave_max_key(cand_key x) {
-#pragma unroll
-  for (int mask = 1; mask < 64; mask <<= 1) {
-    const uint32_t lo = __shfl_xor((uint32_t)x, mask, 64);
-    const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), mask, 64);
-    const cand_key y = ((cand_key)hi << 32) | lo;
-    x = y > x ? y : x;
-  }
-  return x;
+  x = max_stage<0>(x);
+  x = max_stage<1>(x);
+  x = max_stage<2>(x);
+  x = max_stage<3>(x);
+  x = max_stage<4>(x);
+  return max_stage<5>(x);
+}
+
+// Wave-wide log-sum-exp combine of (max, sum exp) pairs; every lane ends
+// with the same result (each stage combines two disjoint lane sets with a
+// commutative merge).
+template <int S>
+__device__ __forceinline__ void lse_stage(float &m, float &s) {
+  uint32_t ma, mb, sa, sb;
+  stage32<S>(__float_as_uint(m), ma, mb);
+  stage32<S>(__float_as_uint(s), sa, sb);
+  float M = __uint_as_float(ma), Sm = __uint_as_float(sa);
+  lse_merge(M, Sm, __uint_as_float(mb), __uint_as_float(sb));
+  m = M;
+  s = Sm;
+}
+__device__ __forceinline__ void wave_lse(float &m, float &s) {
+  lse_stage<0>(m, s);
+  lse_stage<1>(m, s);
+  lse_stage<2>(m, s);
+  lse_stage<3>(m, s);
+  lse_stage<4>(m, s);
+  lse_stage<5>(m, s);
 }
 
 // Merge the per-tile partials of one row (one wave). Each lane folds the
@@ -75,13 +102,7 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
       }
     }
   }
-#pragma unroll
-  for (int mask = 1; mask < 64; mask <<= 1) {
-    const float m2 = __shfl_xor(m, mask, 64), s2 = __shfl_xor(s, mask, 64);
-    lse_merge(m, s, m2, s2);
-  }
-  m = __shfl(m, 0, 64);
-  s = __shfl(s, 0, 64);
+  wave_lse(m, s);
   mine = 0ull;
 #pragma unroll 1
   for (int r = 0; r < k; ++r) {
@@ -118,6 +139,20 @@ __global__ __launch_bounds__(256) void k_rowmerge(DevState st) {
 // key (parent rank << 24 | token + 1; a no-op has token -1).
 __device__ __forceinline__ bool ranks_above(double sa, int ka, double sb, int kb) {
   return sa > sb || (sa == sb && ka < kb);
+}
+
+// One stage of a wave-wide choice of the best (score, key) pair.
+template <int S>
+__device__ __forceinline__ void best_stage(double &bs, int &bk) {
+  const unsigned long long sbits = (unsigned long long)__double_as_longlong(bs);
+  unsigned long long sa, sb;
+  uint32_t ka, kb;
+  stage64<S>(sbits, sa, sb);
+  stage32<S>((uint32_t)bk, ka, kb);
+  const double xa = __longlong_as_double((long long)sa), xb = __longlong_as_double((long long)sb);
+  const bool b_wins = ranks_above(xb, (int)kb, xa, (int)ka);
+  bs = b_wins ? xb : xa;
+  bk = b_wins ? (int)kb : (int)ka;
 }
 
 constexpr int BEAM_THREADS = 512;
@@ -218,15 +253,12 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     for (int r = 0; r < k; ++r) {
       double bs = hs;
       int bk = hk;
-#pragma unroll
-      for (int mask = 1; mask < 64; mask <<= 1) {
-        const double os = __shfl_xor(bs, mask, 64);
-        const int ok = __shfl_xor(bk, mask, 64);
-        if (ranks_above(os, ok, bs, bk)) {
-          bs = os;
-          bk = ok;
-        }
-      }
+      best_stage<0>(bs, bk);
+      best_stage<1>(bs, bk);
+      best_stage<2>(bs, bk);
+      best_stage<3>(bs, bk);
+      best_stage<4>(bs, bk);
+      best_stage<5>(bs, bk);
       if (bk == NO_KEY) break;   // fewer than k candidates
       if (lane == r) {
         rs = bs;
@@ -244,14 +276,15 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     // drop an expansion whose parent already has M kept expansions (no-ops
     // exempt). A parent's kept expansions before rank r are its first M
     // delta-survivors, so the M test needs only their count.
-    const double ref = __shfl(rs, 0, 64);
+    const double ref = __longlong_as_double(((long long)__builtin_amdgcn_readlane((int)(__double_as_longlong(rs) >> 32), 0) << 32) |
+                                            (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(rs), 0));
     const int rpar = rk >> 24, rtok = (rk & 0xFFFFFF) - 1;
     const bool keepd = lane < nfull && !(rs < ref - st.delta);
     int before = 0;
 #pragma unroll 1
     for (int o = 0; o < nfull; ++o) {
-      const int okk = __shfl(rk, o, 64);
-      const int okeep = __shfl((int)keepd, o, 64);
+      const int okk = __builtin_amdgcn_readlane(rk, o);
+      const int okeep = __builtin_amdgcn_readlane((int)keepd, o);
       before += (o < lane && okeep && (okk >> 24) == rpar && (okk & 0xFFFFFF) != 0);
     }
     const bool kept = keepd && (rtok < 0 || before < st.M);

@@ -20,6 +20,7 @@
 
 #include "mfma_common.h"
 #include "topk.h"
+#include "wave.h"
 
 namespace sb {
 namespace {
@@ -225,11 +226,19 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
       bitonic_sort_desc<16>(keys);
 #pragma unroll
       for (int q = 0; q < KB; ++q) tks[bl].k[q] = keys[q];
-      TopK<KB> o;
-      topk_shfl_xor(o, tks[bl], 32);
-      const float m2 = __shfl_xor(m, 32, 64), s2 = __shfl_xor(s, 32, 64);
-      lse_merge(m, s, m2, s2);
-      topk_merge(tks[bl], o);
+      // Lanes l and l+32 hold the same row: combine their lists and sums
+      // (both lanes get the same result).
+      TopK<KB> lo, hi;
+#pragma unroll
+      for (int q = 0; q < KB; ++q) stage64<5>(tks[bl].k[q], lo.k[q], hi.k[q]);
+      topk_merge(lo, hi);
+      tks[bl] = lo;
+      uint32_t ma, mb, sa, sb;
+      stage32<5>(__float_as_uint(m), ma, mb);
+      stage32<5>(__float_as_uint(s), sa, sb);
+      m = __uint_as_float(ma);
+      s = __uint_as_float(sa);
+      lse_merge(m, s, __uint_as_float(mb), __uint_as_float(sb));
       ms[bl] = m;
       ss[bl] = s;
     }
