@@ -55,6 +55,17 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rowbytes = d * 4;
   const int kq = d / RSPLIT;                       // K range of this wave (multiple of 8)
+  // Epilogue mapping: thread -> row j = tid/16, features 2*(tid%16)..+1. Its
+  // embedding values are fetched before the K loop so that their latency
+  // overlaps the GEMM.
+  const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
+  const int row = r0 + j;
+  float ev[2] = {0.0f, 0.0f};
+  if (row < R) {
+    const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
+    ev[0] = E[0];
+    ev[1] = E[1];
+  }
   const float *arow = static_cast<const float *>(st.W_h) + (size_t)(v0 + (lane & 31)) * d + w * kq;
   const float *brow = reinterpret_cast<const float *>(rec_state_row(st, r0 + (lane & 31), R, rowbytes)) + w * kq;
   const int h = (lane >> 5) * 4;
@@ -74,11 +85,7 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
     red[w][(lane & 31) * RT + i] = acc[reg];
   }
   __syncthreads();
-  // 512 threads x 2 outputs: thread -> row j = tid/16, features 2*(tid%16)..+1.
-  const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
-  const int row = r0 + j;
   if (row < R) {
-    const float *E = static_cast<const float *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
     float hv[2];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -86,7 +93,7 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
       float pre = red[0][o];
 #pragma unroll
       for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
-      hv[q] = tanhf(pre + E[q]);
+      hv[q] = tanhf(pre + ev[q]);
     }
     float *out = static_cast<float *>(st.hbuf) + (size_t)row * d + v0 + i0;
     out[0] = hv[0];
@@ -106,6 +113,11 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
   const int rowbytes = d * 2;
   const int kq = d / RSPLIT;                       // multiple of 16
   const int r16 = lane & 15, g = lane >> 4;
+  const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
+  const int row = r0 + j;
+  uint32_t ev = 0u;   // embedding pair, fetched before the K loop
+  if (row < R)
+    ev = *reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0);
   // A: 2 blocks of 16 out features, B: 2 blocks of 16 rows; the lane feeds
   // 4 consecutive bf16 at k = kk + 4g to 4 MFMAs (same permutation for A, B).
   const uint16_t *a0 = static_cast<const uint16_t *>(st.W_h) + (size_t)(v0 + r16) * d + w * kq + 4 * g;
@@ -150,10 +162,7 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
         red[w][j * RT + i] = acc[x][y][q];
       }
   __syncthreads();
-  const int j = threadIdx.x >> 4, i0 = (threadIdx.x & 15) * 2;
-  const int row = r0 + j;
   if (row < R) {
-    const uint16_t *E = static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0;
     uint16_t hb[2];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -161,7 +170,7 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
       double pre = red[0][o];
 #pragma unroll
       for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
-      hb[q] = bf16_rne_from_double(tanh(pre + (double)bf16f(E[q])));
+      hb[q] = bf16_rne_from_double(tanh(pre + (double)bf16f((uint16_t)(q ? ev >> 16 : ev & 0xFFFFu))));
     }
     *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + v0 + i0) =
         (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
