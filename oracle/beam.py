@@ -48,6 +48,12 @@ class StepResult:
     full: List[tuple]           # the full beam B' as (score, parent, token)
 
 
+def rank_key(e):
+    """Ranking key of an expansion (score, parent rank, token): higher score
+    first, then lower parent rank, then lower token (a no-op has -1)."""
+    return (-e[0], e[1], e[2])
+
+
 def _top_children(lp_row: np.ndarray, keep: int) -> np.ndarray:
     """Indices of every token whose lp is >= the keep-th largest lp (ties
     included, so that the exact key order can be applied afterwards)."""
@@ -78,7 +84,7 @@ def beam_step(beam: List[Cand], lp: dict, h_new: dict, t: int, max_len: int,
                 pool.append((c.score + float(row[w]), j, int(w)))
         else:
             pool.append((c.score, j, NOOP_TOKEN))
-    pool.sort(key=lambda e: (-e[0], e[1], e[2]))
+    pool.sort(key=rank_key)
     full = pool[:k]
 
     # Margins of every ranking decision: adjacent pairs inside the full beam
@@ -119,3 +125,56 @@ def beam_step(beam: List[Cand], lp: dict, h_new: dict, t: int, max_len: int,
                              h_new[j] if st == ACTIVE else None, w))
     ended = not any(c.status == ACTIVE for c in new_beam)
     return StepResult(new_beam, ended, float(margin), full)
+
+
+@dataclasses.dataclass
+class FairseqStepResult:
+    beam: List[Cand]            # the next beam: active candidates only, rank order
+    outputs: List[Cand]         # candidates finalized at this step, in rank order
+    margin: float
+
+
+def beam_step_fairseq(beam: List[Cand], lp: dict, h_new: dict, t: int, max_len: int,
+                      k: int, n_out: int, eos: int = 0) -> FairseqStepResult:
+    """One step under the Fixed-Fairseq finalization rule (App. A.1, the
+    implementation difference to Fairseq): a terminated candidate that
+    enters the full beam B' (the best k expansions) is added to the list of
+    final outputs at once, instead of staying on the beam where it could be
+    displaced later. The beam itself keeps k active candidates: the first k
+    active expansions in rank order. Fixed width: no threshold, no M.
+
+    beam  : active candidates in rank order; n_out: outputs collected so far.
+    Outputs beyond k in total are not taken.
+    """
+    pool = []
+    for j, c in enumerate(beam):
+        row = lp[j]
+        # Each parent has one EOS child at most, so its best k+1 children
+        # cover both B' and the first k active children.
+        for w in _top_children(row, k + 1):
+            pool.append((c.score + float(row[w]), j, int(w)))
+    pool.sort(key=rank_key)
+    # Decisions: membership and order of B' and of the first k active
+    # children all lie within the first 2k + 1 ranks.
+    margin = np.inf
+    head = pool[:2 * k + 1]
+    for a, b in zip(head, head[1:]):
+        margin = min(margin, a[0] - b[0])
+
+    def terminated(w):
+        return w == eos or t == max_len
+
+    outputs = []
+    for score, j, w in pool[:k]:
+        if terminated(w) and n_out + len(outputs) < k:
+            p = beam[j]
+            outputs.append(Cand(score, p.tokens + (w,), EOS if w == eos else MAXLEN, None, w))
+    new_beam = []
+    for score, j, w in pool:
+        if len(new_beam) == k:
+            break
+        if terminated(w):
+            continue
+        p = beam[j]
+        new_beam.append(Cand(score, p.tokens + (w,), ACTIVE, h_new[j], w))
+    return FairseqStepResult(new_beam, outputs, float(margin))

@@ -26,7 +26,7 @@ from typing import Callable, Dict, List, Optional, Sequence
 
 import numpy as np
 
-from .beam import ACTIVE, Cand, beam_step
+from .beam import ACTIVE, Cand, beam_step, beam_step_fairseq
 
 
 @dataclasses.dataclass
@@ -66,12 +66,13 @@ class _Beam:
     input: int
     steps: int
     cands: List[Cand]
+    outputs: List[Cand] = dataclasses.field(default_factory=list)   # Fixed-Fairseq rule only
 
 
 def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
            n: int, eps: float, k: int, delta: float = math.inf,
            M: Optional[int] = None, on_step: Optional[Callable] = None,
-           select: str = "min_steps") -> SearchResult:
+           select: str = "min_steps", rule: str = "paper") -> SearchResult:
     """Run Alg. 1 over inputs 0..N-1 (h0[i] is e_i = E(x_i)).
 
     `decoder` needs initial_state(h0_row) and expand(h_prev, y, t, Lx) ->
@@ -80,10 +81,16 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
     schedule. `select` is Alg. 1's beam selection, "min_steps" (the beams
     with minimal l_t), or "fifo" for Var-Str-FIFO (App. A, alternative
     method analysis: beams up to the batch capacity n, starting from the
-    one with maximal l_t).
+    one with maximal l_t). `rule` is the finalization rule: "paper"
+    (App. A.1: terminated candidates stay on the beam) or "fairseq"
+    (App. A.1's Fixed-Fairseq: they are output at once; fixed width, so
+    delta and M are not applied); a beam under the Fairseq rule finishes
+    with k outputs, kept in the order they were finalized.
     """
     if select not in ("min_steps", "fifo"):
         raise ValueError(select)
+    if rule not in ("paper", "fairseq"):
+        raise ValueError(rule)
     N = len(Lx)
     M = k if M is None else int(M)
     if not (k >= 1 and n >= 1 and 0.0 <= eps < 1.0 and 1 <= M <= k):
@@ -134,15 +141,27 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
         finished = []
         for bi, b in enumerate(sel):
             res.noops += sum(1 for cand in b.cands if cand.status != ACTIVE)
-            out = beam_step(b.cands, per_beam_lp.get(bi, {}), per_beam_h.get(bi, {}),
-                            b.steps + 1, int(max_len[b.input]), k, delta, M)
             res.widths[b.input].append(sum(1 for cand in b.cands if cand.status == ACTIVE))
-            res.margins[b.input].append(out.margin)
-            res.min_margin[b.input] = min(res.min_margin[b.input], out.margin)
-            b.cands = out.beam
+            if rule == "fairseq":
+                fo = beam_step_fairseq(b.cands, per_beam_lp.get(bi, {}), per_beam_h.get(bi, {}),
+                                       b.steps + 1, int(max_len[b.input]), k, len(b.outputs))
+                b.outputs += fo.outputs
+                b.cands = fo.beam
+                margin = fo.margin
+                ended = len(b.outputs) >= k or not fo.beam
+                final = b.outputs
+            else:
+                out = beam_step(b.cands, per_beam_lp.get(bi, {}), per_beam_h.get(bi, {}),
+                                b.steps + 1, int(max_len[b.input]), k, delta, M)
+                b.cands = out.beam
+                margin = out.margin
+                ended = out.ended
+                final = out.beam
+            res.margins[b.input].append(margin)
+            res.min_margin[b.input] = min(res.min_margin[b.input], margin)
             b.steps += 1
-            if out.ended:
-                res.hyps[b.input] = [Hyp(cd.tokens, cd.score, cd.status) for cd in out.beam]
+            if ended:
+                res.hyps[b.input] = [Hyp(cd.tokens, cd.score, cd.status) for cd in final]
                 res.finalize_step[b.input] = res.timesteps
                 res.steps_taken[b.input] = b.steps
                 finished.append(b)
@@ -155,8 +174,8 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
 def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var_stream",
                     inputs: Optional[Sequence[int]] = None, decoder=None) -> SearchResult:
     """Convenience wrapper: decode (a subset of) a synthgen Workload with its
-    config's parameters; `sched` picks Fixed / Var-Batch / Var-Stream /
-    Var-Str-FIFO ("var_fifo")."""
+    config's parameters; `sched` picks Fixed / Fixed-Stream / Fixed-Fairseq /
+    Var-Batch / Var-Stream / Var-Str-FIFO ("var_fifo")."""
     from .decoder import ElmanDecoder
     c = wl.cfg
     dec = decoder or ElmanDecoder.from_workload(wl)
@@ -165,12 +184,17 @@ def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var
     eps = c.eps if eps is None else eps
     delta = c.delta if delta is None else delta
     M = c.M if M is None else M
+    rule = "paper"
     if sched == "fixed":
         eps, delta, M = 0.0, math.inf, k
+    elif sched == "fixed_stream":          # App. A.1 / Table 3: Fixed with streaming refill
+        delta, M = math.inf, k
+    elif sched == "fixed_fairseq":         # App. A.1: Fairseq's finalization rule
+        eps, delta, M, rule = 0.0, math.inf, k, "fairseq"
     elif sched == "var_batch":
         eps = 0.0
     elif sched not in ("var_stream", "var_fifo"):
         raise ValueError(sched)
     idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
     return decode(dec, wl.h0[idx], wl.Lx[idx], wl.max_len[idx], n, eps, k, delta, M,
-                  select="fifo" if sched == "var_fifo" else "min_steps")
+                  select="fifo" if sched == "var_fifo" else "min_steps", rule=rule)

@@ -45,6 +45,8 @@ PINS = {
     "max_per_node": lambda: tsearch.test_scripted_cases(_cases()["max_candidates_per_node_and_maxlen"]),
     "noop": lambda: tsearch.test_scripted_cases(_cases()["noop_keeps_terminated_rank"]),
     "ties": lambda: tsearch.test_scripted_cases(_cases()["exact_ties_follow_rank_key"]),
+    "fairseq": lambda: tsearch.test_scripted_cases(_cases()["fairseq_outputs_terminated_immediately"]),
+    "fairseq_exhaustive": lambda: tsearch.test_fairseq_rule_exhaustive(3, 4, 1),
     "fig1": tsearch.test_fig1_schedule,
     "stream_vs_batch": lambda: tsearch.test_var_stream_matches_var_batch(0, 4, 0.25),
 }
@@ -66,10 +68,14 @@ MUTATIONS = [
     ("max_per_node_ignored", "beam", "if per_parent.get(j, 0) >= M:", "if False:", ["max_per_node"]),
     ("maxlen_off_by_one", "beam", "elif t == max_len:", "elif t == max_len - 1:",
      ["max_per_node", "exhaustive"]),
-    ("parent_rank_tiebreak_reversed", "beam", "pool.sort(key=lambda e: (-e[0], e[1], e[2]))",
-     "pool.sort(key=lambda e: (-e[0], -e[1], e[2]))", ["ties"]),
-    ("token_tiebreak_reversed", "beam", "pool.sort(key=lambda e: (-e[0], e[1], e[2]))",
-     "pool.sort(key=lambda e: (-e[0], e[1], -e[2]))", ["ties"]),
+    ("parent_rank_tiebreak_reversed", "beam", "return (-e[0], e[1], e[2])",
+     "return (-e[0], -e[1], e[2])", ["ties"]),
+    ("token_tiebreak_reversed", "beam", "return (-e[0], e[1], e[2])",
+     "return (-e[0], e[1], -e[2])", ["ties"]),
+    ("fairseq_outputs_beyond_full_beam", "beam", "for score, j, w in pool[:k]:",
+     "for score, j, w in pool[:2 * k]:", ["fairseq"]),
+    ("fairseq_beam_keeps_terminated", "beam", "        if terminated(w):\n            continue\n", "",
+     ["fairseq", "fairseq_exhaustive"]),
     ("refill_strict", "search", "len(live) <= eps * n", "len(live) < eps * n", ["fig1"]),
     ("expand_all_live", "search", "sel = [b for b in live if b.steps == lmin]", "sel = list(live)", ["fig1"]),
     ("bias_uses_global_timestep", "search", "t = np.array([sel[bi].steps + 1 for bi, _ in rows])",
@@ -87,6 +93,7 @@ def test_planted_mistake_is_caught(monkeypatch, name, modname, old, new, pins):
                     monkeypatch.setattr(target, attr, getattr(mut, attr))
     elif modname == "beam":
         monkeypatch.setattr(oracle.search, "beam_step", mut.beam_step)
+        monkeypatch.setattr(oracle.search, "beam_step_fairseq", mut.beam_step_fairseq)
     else:
         for attr in ("decode", "decode_workload"):
             monkeypatch.setattr(tsearch, attr, getattr(mut, attr))

@@ -66,16 +66,68 @@ def test_k1_is_greedy(seed):
         assert abs(res.hyps[i][0].score - sc) < 1e-12
 
 
-def test_scores_are_teacher_forced_sums():
+@pytest.mark.parametrize("sched", ["var_stream", "fixed_fairseq"])
+def test_scores_are_teacher_forced_sums(sched):
     # Every output's score is the sum of its per-token log-probabilities
     # (Sec. 2), recomputed token by token from h0.
     wl = make_workload(scaled(1, N=12, V=50, d=16))
-    res = decode_workload(wl)
+    res = decode_workload(wl, sched=sched)
     c = wl.cfg
     for i in range(12):
         for h in res.hyps[i]:
             s = brute.score_tokens(wl.W_h, wl.E, wl.W_out, c.beta, False, wl.h0[i], wl.Lx[i], h.tokens)
             assert abs(s - h.score) < 1e-10
+
+
+@pytest.mark.parametrize("V,max_len,seed", [(2, 5, 0), (3, 4, 1), (4, 4, 2)])
+def test_fairseq_rule_exhaustive(V, max_len, seed):
+    # Fixed-Fairseq rule (App. A.1) with k >= the number of complete outputs:
+    # every expansion enters the full beam B', so every complete output is
+    # finalized (terminated ones at once) and the beam never drops an active
+    # prefix; Y is every complete output (in the order finalized).
+    d = 4
+    model = tiny_model(V, d, seed, False)
+    rng = np.random.default_rng(200 + seed)
+    h0 = rng.standard_normal((1, d))
+    allseq = brute.enumerate_complete(*model, h0[0], 2, max_len)
+    res = decode(ElmanDecoder(*model), h0, [2], [max_len], n=1, eps=0.0, k=len(allseq), rule="fairseq")
+    got = sorted(((h.tokens, h.score, h.status) for h in res.hyps[0]), key=lambda e: -e[1])
+    want = sorted(allseq, key=lambda e: -e[1])
+    assert len(got) == len(want)
+    for g, w in zip(got, want):
+        assert g[0] == w[0] and g[2] == w[2] and abs(g[1] - w[1]) < 1e-12
+    # Finalization order: nondecreasing length (outputs of a step come after
+    # those of earlier steps).
+    lens = [len(h.tokens) for h in res.hyps[0]]
+    assert lens == sorted(lens)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_fairseq_rule_k1_is_greedy(seed):
+    # k = 1: B' is the single best expansion; it is output if terminated,
+    # else it is the whole next beam -- the greedy argmax chain (Sec. 2).
+    V, d = 9, 6
+    model = tiny_model(V, d, seed, beta=0.3)
+    rng = np.random.default_rng(seed)
+    h0 = rng.standard_normal((4, d))
+    Lx, ml = [3, 5, 8, 2], [10, 12, 6, 9]
+    res = decode(ElmanDecoder(*model), h0, Lx, ml, n=2, eps=0.5, k=1, rule="fairseq")
+    for i in range(4):
+        toks, sc = brute.greedy(*model, h0[i], Lx[i], ml[i])
+        assert len(res.hyps[i]) == 1
+        assert res.hyps[i][0].tokens == toks and abs(res.hyps[i][0].score - sc) < 1e-12
+
+
+def test_fairseq_rule_streaming_matches_batch():
+    # Results are per input (Sec. 3), so streaming the Fixed-Fairseq search
+    # returns Fixed-Fairseq's outputs; every input gets k outputs.
+    wl = make_workload(scaled(1, N=17, V=40, d=10, len_hi=9))
+    a = decode_workload(wl, n=4, sched="fixed_fairseq")
+    b = decode(ElmanDecoder.from_workload(wl), wl.h0, wl.Lx, wl.max_len, n=4, eps=0.5,
+               k=wl.cfg.k, rule="fairseq")
+    _same_outputs(a, b)
+    assert a.expansions == b.expansions and a.noops == 0
+    assert all(len(y) == wl.cfg.k for y in a.hyps)
 
 
 def _load_cases():
@@ -90,7 +142,7 @@ def test_scripted_cases(case):
     dec = PrefixDecoder(table, case["V"])
     delta = math.inf if case["delta"] is None else case["delta"]
     res = decode(dec, np.zeros((1, 1)), [0], [case["max_len"]], n=1, eps=0.0,
-                 k=case["k"], delta=delta, M=case["M"])
+                 k=case["k"], delta=delta, M=case["M"], rule=case.get("rule", "paper"))
     got = [(list(h.tokens), h.status, h.score) for h in res.hyps[0]]
     assert len(got) == len(case["expect"])
     for g, (toks, st, p) in zip(got, case["expect"]):
