@@ -108,7 +108,9 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--sched", default="var_stream", choices=["fixed", "var_batch", "var_stream", "var_fifo"])
+    ap.add_argument("--sched", default="var_stream",
+                    choices=["fixed", "fixed_stream", "fixed_fairseq", "fixed_fairseq_stream", "var_batch",
+                             "var_stream", "var_fifo"])
     ap.add_argument("--eps", type=float, default=None)
     ap.add_argument("--cpu-sample", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -132,7 +134,7 @@ def main():
 
     cfg = get_config(args.config)
     eps = cfg.eps if args.eps is None else args.eps
-    if args.sched not in ("var_stream", "var_fifo"):
+    if args.sched not in ("var_stream", "var_fifo", "fixed_stream", "fixed_fairseq_stream"):
         eps = 0.0
     wl = make_workload(cfg)
     weights = weights_to_device(wl)

@@ -55,7 +55,19 @@ typedef enum {
  * timestep (the batch capacity n taken from the beam with the most steps
  * down; at most n beams are live). All four return the same outputs for
  * the same parameters (eps, delta, M as forced below). */
-typedef enum { SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2, SB_VAR_FIFO = 3 } sb_sched;
+typedef enum { SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2, SB_VAR_FIFO = 3, SB_FIXED_STREAM = 4 } sb_sched;
+/* SB_FIXED_STREAM (App. A.1, Table 3): fixed-width search (delta=+inf, M=k)
+ * with Var-Stream's refill and selection; its outputs equal SB_FIXED's. */
+
+/* Finalization rule (App. A.1, implementation differences to Fairseq).
+ * SB_RULE_PAPER: terminated candidates stay on the beam through no-op
+ * expansions, are output once nothing active ranks above them, and may be
+ * displaced meanwhile; Y[i] is the final beam in rank order.
+ * SB_RULE_FAIRSEQ: a terminated candidate entering the best k expansions is
+ * output at once; the beam keeps the k best active expansions; the input
+ * finishes with k outputs, Y[i] in the order they were finalized. Fixed
+ * width: delta and M are not applied. Needs k <= 15. */
+typedef enum { SB_RULE_PAPER = 0, SB_RULE_FAIRSEQ = 1 } sb_rule;
 
 /* Storage type of weights, h0 and decoder states. SB_F32: fp32 everywhere
  * (MFMA fp32, fp32 accumulation). SB_BF16: bf16 weights and states; the
@@ -75,9 +87,11 @@ typedef struct {
                             score(best) - delta; +inf disables (Sec. 4, App. A.3) */
   int32_t max_per_node;  /* M: max kept expansions per parent per step, 1..k      */
   int32_t sched;         /* sb_sched; SB_FIXED forces eps=0, delta=+inf, M=k;
+                            SB_FIXED_STREAM forces delta=+inf, M=k;
                             SB_VAR_BATCH forces eps=0                             */
   int32_t max_len_cap;   /* upper bound on every input's max_len, 1..4096         */
   int32_t max_inputs;    /* queue capacity (inputs per decoder lifetime/reset)    */
+  int32_t finalize_rule; /* sb_rule; SB_RULE_FAIRSEQ forces delta=+inf, M=k       */
 } sb_params;
 
 /* Synthetic decoder D (Sec. 2). Token 0 is EOS and also the start symbol.
@@ -101,7 +115,8 @@ typedef struct {
 /* One finalized hypothesis y_ij of Y[i] (Alg. 1 output). */
 typedef struct {
   int64_t input;         /* queue position of its input (submission order)         */
-  int32_t rank;          /* position in Y[i] (0 = best)                            */
+  int32_t rank;          /* position in Y[i]: rank order (0 = best) under the
+                            paper's rule, finalization order under Fairseq's      */
   int32_t length;        /* number of tokens, EOS included when present            */
   int32_t status;        /* SB_HYP_EOS or SB_HYP_MAXLEN                             */
   int32_t finalize_step; /* global timestep at which its beam finished            */

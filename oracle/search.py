@@ -191,6 +191,8 @@ def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var
         delta, M = math.inf, k
     elif sched == "fixed_fairseq":         # App. A.1: Fairseq's finalization rule
         eps, delta, M, rule = 0.0, math.inf, k, "fairseq"
+    elif sched == "fixed_fairseq_stream":  # the same rule with the streaming refill
+        delta, M, rule = math.inf, k, "fairseq"
     elif sched == "var_batch":
         eps = 0.0
     elif sched not in ("var_stream", "var_fifo"):

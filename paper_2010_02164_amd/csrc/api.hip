@@ -46,7 +46,7 @@ namespace {
 constexpr size_t ALIGN = 256;
 
 struct Layout {
-  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, s_status, s_score, s_tok, s_h,
+  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, s_status, s_score, s_tok, s_h,
       s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
       o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, wout_t, total;
 };
@@ -60,7 +60,8 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   const size_t es = m.dtype == SB_BF16 ? 2 : 4;
   const size_t n = p.n, k = p.k, d = m.d, nk = n * k, Rm = nk;
   const size_t S = proj_tiles(m.vocab);
-  const size_t KB = kbucket_of(p.k);
+  const size_t KB = kbucket_of(p.k + (p.finalize_rule == SB_RULE_FAIRSEQ ? 1 : 0));
+  const size_t bpw = p.finalize_rule == SB_RULE_FAIRSEQ ? 2 * (size_t)p.k : (size_t)p.k;
   const size_t Q = p.max_inputs, MLC = p.max_len_cap;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -77,13 +78,14 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.b_sel = take(n * 4);
   L.b_par = take(n * 4);
   L.b_ml = take(n * 4);
+  L.b_nout = take(n * 4);
   L.s_status = take(nk * 4);
   L.s_score = take(nk * 8);
   L.s_tok = take(nk * 4);
   L.s_h = take(nk * d * es);
   L.s_row = take(nk * 4);
   L.s_prow = take(nk * 4);
-  L.bp = take(Q * MLC * k * 4);
+  L.bp = take(Q * MLC * bpw * 4);
   L.r_slot = take(Rm * 4);
   L.r_hsrc = take(Rm * 4);
   L.r_y = take(Rm * 4);
@@ -125,7 +127,11 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   if (!(p->eps >= 0.0 && p->eps < 1.0)) return bad(SB_E_INVALID_ARG, "eps must be in [0, 1)");
   if (!(p->delta > 0.0)) return bad(SB_E_INVALID_ARG, "delta must be > 0 (use +inf to disable)");
   if (p->max_per_node < 1 || p->max_per_node > p->k) return bad(SB_E_INVALID_ARG, "max_per_node must be in [1, k]");
-  if (p->sched < SB_FIXED || p->sched > SB_VAR_FIFO) return bad(SB_E_INVALID_ARG, "unknown scheduler");
+  if (p->sched < SB_FIXED || p->sched > SB_FIXED_STREAM) return bad(SB_E_INVALID_ARG, "unknown scheduler");
+  if (p->finalize_rule != SB_RULE_PAPER && p->finalize_rule != SB_RULE_FAIRSEQ)
+    return bad(SB_E_INVALID_ARG, "unknown finalization rule");
+  if (p->finalize_rule == SB_RULE_FAIRSEQ && p->k > KMAX_SUPPORTED - 1)
+    return bad(SB_E_UNSUPPORTED, "the Fairseq rule needs k <= 15");
   if (p->max_len_cap < 1 || p->max_len_cap > 4096) return bad(SB_E_INVALID_ARG, "max_len_cap must be in [1, 4096]");
   if (p->max_inputs < 1) return bad(SB_E_INVALID_ARG, "max_inputs must be >= 1");
   const int64_t es = m->dtype == SB_BF16 ? 2 : 4;
@@ -146,6 +152,13 @@ sb_params effective(const sb_params &p) {
     e.max_per_node = p.k;
   } else if (p.sched == SB_VAR_BATCH) {
     e.eps = 0.0;
+  } else if (p.sched == SB_FIXED_STREAM) {
+    e.delta = INFINITY;
+    e.max_per_node = p.k;
+  }
+  if (p.finalize_rule == SB_RULE_FAIRSEQ) {
+    e.delta = INFINITY;
+    e.max_per_node = p.k;
   }
   return e;
 }
@@ -282,6 +295,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.b_sel = reinterpret_cast<int32_t *>(w + L.b_sel);
   st.b_par = reinterpret_cast<int32_t *>(w + L.b_par);
   st.b_ml = reinterpret_cast<int32_t *>(w + L.b_ml);
+  st.b_nout = reinterpret_cast<int32_t *>(w + L.b_nout);
   st.s_status = reinterpret_cast<int32_t *>(w + L.s_status);
   st.s_score = reinterpret_cast<double *>(w + L.s_score);
   st.s_tok = reinterpret_cast<int32_t *>(w + L.s_tok);
@@ -325,7 +339,9 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.dtype = model->dtype;
   st.kv_layers = model->kv_layers;
   st.max_inputs = p.max_inputs;
-  st.kbucket = kbucket_of(p.k);
+  st.rule = p.finalize_rule;
+  st.bpw = p.finalize_rule == SB_RULE_FAIRSEQ ? 2 * p.k : p.k;
+  st.kbucket = kbucket_of(p.k + st.rule);   // the Fairseq rule draws k+1 children per parent
   st.hist_width = std::max(16, (st.R_max + 63) / 64);
   st.select_all = p.sched == SB_VAR_FIFO ? 1 : 0;
   {
@@ -625,14 +641,14 @@ sb_status sb_debug_slot(sb_decoder *dec, int32_t beam, int32_t rank, int32_t *st
   *n_tokens = 0;
   if (bin < 0 || sst == SLOT_EMPTY) return SB_OK;
   // Tokens: walk this input's backpointers from level `steps`.
-  std::vector<uint32_t> bp((size_t)st.max_len_cap * st.k);
-  HIPCHK(hipMemcpyAsync(bp.data(), st.bp + (size_t)bin * st.max_len_cap * st.k, bp.size() * 4,
+  std::vector<uint32_t> bp((size_t)st.max_len_cap * st.bpw);
+  HIPCHK(hipMemcpyAsync(bp.data(), st.bp + (size_t)bin * st.max_len_cap * st.bpw, bp.size() * 4,
                         hipMemcpyDeviceToHost, dec->stream));
   HIPCHK(hipStreamSynchronize(dec->stream));
   std::vector<int32_t> rev;
   int pos = rank;
   for (int lev = bst; lev >= 1; --lev) {
-    const uint32_t e = bp[(size_t)(lev - 1) * st.k + pos];
+    const uint32_t e = bp[(size_t)(lev - 1) * st.bpw + pos];
     if ((e & 0xFFFFFFu) != BP_NOOP) rev.push_back((int32_t)(e & 0xFFFFFFu));
     pos = (int)(e >> 24);
   }

@@ -159,6 +159,16 @@ constexpr int BEAM_THREADS = 512;
 constexpr int BEAM_WAVES = BEAM_THREADS / 64;
 constexpr int NO_KEY = 0x7FFFFFFF;
 
+// Draw the best remaining head (score, key) over the wave; every lane gets it.
+__device__ __forceinline__ void wave_best(double &bs, int &bk) {
+  best_stage<0>(bs, bk);
+  best_stage<1>(bs, bk);
+  best_stage<2>(bs, bk);
+  best_stage<3>(bs, bk);
+  best_stage<4>(bs, bk);
+  best_stage<5>(bs, bk);
+}
+
 template <int KB>
 __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const int b = blockIdx.x;
@@ -166,6 +176,8 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const int wave = tid >> 6, lane = tid & 63;
   const int k = st.k;
   const int base = b * k;
+  const bool fairseq = st.rule == 1;
+  const int KC = k + (fairseq ? 1 : 0);   // children drawn per parent
   // Everything the beam needs from its records is loaded in one round,
   // before the selection flag is tested.
   int my_status = SLOT_EMPTY, my_row = -1;
@@ -175,24 +187,26 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     my_row = st.s_row[base + tid];
     my_score = st.s_score[base + tid];
   }
-  int my_q = 0, my_t = 0, my_ml = 0;
+  int my_q = 0, my_t = 0, my_ml = 0, my_nout = 0;
   if (tid == 64) {
     my_q = st.b_input[b];
     my_t = st.b_steps[b] + 1;     // 1-based index of the emitted token
     my_ml = st.b_ml[b];
+    my_nout = st.b_nout[b];
   }
   // b_sel is cleared for every beam when nothing is live (R == 0).
   if (!st.b_sel[b]) return;
   __shared__ int sl_status[KMAX_SUPPORTED], sl_row[KMAX_SUPPORTED];
   __shared__ double sl_score[KMAX_SUPPORTED];
-  __shared__ int q_in_sh, t_sh, max_len_sh;
-  // Best k log-probabilities and tokens of each active parent's row.
+  __shared__ int q_in_sh, t_sh, max_len_sh, nout_sh;
+  // Best KC log-probabilities and tokens of each active parent's row.
   __shared__ double ch_lp[KMAX_SUPPORTED * KMAX_SUPPORTED];
   __shared__ int ch_tok[KMAX_SUPPORTED * KMAX_SUPPORTED];
-  // The pruned new beam, in rank order.
-  __shared__ double nscore[KMAX_SUPPORTED];
+  // The new beam, in rank order, and (Fairseq rule) this step's outputs.
+  __shared__ double nscore[KMAX_SUPPORTED], oscore[KMAX_SUPPORTED];
   __shared__ int npar[KMAX_SUPPORTED], ntok[KMAX_SUPPORTED], nstat[KMAX_SUPPORTED];
-  __shared__ int nw_sh, nact_sh;
+  __shared__ int opar[KMAX_SUPPORTED], otok[KMAX_SUPPORTED], ostat[KMAX_SUPPORTED];
+  __shared__ int nw_sh, nact_sh, no_sh;
   if (tid < k) {
     sl_status[tid] = my_status;
     sl_row[tid] = my_row;
@@ -202,29 +216,30 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     q_in_sh = my_q;
     t_sh = my_t;
     max_len_sh = my_ml;
+    nout_sh = my_nout;
   }
   __syncthreads();
-  const int q_in = q_in_sh, t = t_sh, max_len = max_len_sh;
+  const int q_in = q_in_sh, t = t_sh, max_len = max_len_sh, nout0 = nout_sh;
 
   // Row merge of every active parent: wave w takes parents w, w+8.
   for (int par = wave; par < k; par += BEAM_WAVES) {
     if (sl_status[par] != SLOT_ACTIVE) continue;
     cand_key mine;
-    const double lse = merge_row<KB>(st, sl_row[par], lane, k, mine);
-    if (lane < k) {
-      ch_lp[par * k + lane] = (double)key_val(mine) - lse;
-      ch_tok[par * k + lane] = key_idx(mine);
+    const double lse = merge_row<KB>(st, sl_row[par], lane, KC, mine);
+    if (lane < KC) {
+      ch_lp[par * KC + lane] = (double)key_val(mine) - lse;
+      ch_tok[par * KC + lane] = key_idx(mine);
     }
   }
   __syncthreads();
 
   if (wave == 0) {
-    // Full beam B' (Sec. 2): the best k of the k|V| expansions plus one
-    // no-op per terminated candidate. Each parent's expansions arrive
-    // sorted, so B' is a k-way merge: lane p < k holds the head of parent
-    // p's list, lane k + p the no-op of parent p; each round takes the
-    // best head (wave maximum) and its lane advances.
-    const bool is_list = lane < k, is_noop = lane >= k && lane < 2 * k;
+    // Each parent's expansions arrive sorted, so the ranking of all
+    // expansions (key: score, parent rank, token) is a k-way merge: lane
+    // p < k holds the head of parent p's list, lane k + p the no-op of a
+    // terminated parent p (paper rule only); each round takes the best head
+    // (wave maximum) and its lane advances. Lane r keeps the entry of rank r.
+    const bool is_list = lane < k, is_noop = !fairseq && lane >= k && lane < 2 * k;
     const int p = is_list ? lane : lane - k;
     const int pstat = (is_list || is_noop) ? sl_status[p] : SLOT_EMPTY;
     int hp = 0;
@@ -234,10 +249,10 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     auto head = [&]() {
       hs = -INFINITY;
       hk = NO_KEY;
-      if (is_list && pstat == SLOT_ACTIVE && hp < k) {
-        const int tok = ch_tok[p * k + hp];
+      if (is_list && pstat == SLOT_ACTIVE && hp < KC) {
+        const int tok = ch_tok[p * KC + hp];
         if (tok >= 0 && tok < st.V) {
-          hs = sl_score[p] + ch_lp[p * k + hp];
+          hs = sl_score[p] + ch_lp[p * KC + hp];
           hk = (p << 24) | (tok + 1);
         }
       } else if (noop_left) {
@@ -246,97 +261,176 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
       }
     };
     head();
-    double rs = -INFINITY;   // lane r: the entry of rank r
+    double rs = -INFINITY;
     int rk = NO_KEY;
     int nfull = 0;
+    if (!fairseq) {
+      // Full beam B' (Sec. 2): the best k expansions, no-ops included.
 #pragma unroll 1
-    for (int r = 0; r < k; ++r) {
-      double bs = hs;
-      int bk = hk;
-      best_stage<0>(bs, bk);
-      best_stage<1>(bs, bk);
-      best_stage<2>(bs, bk);
-      best_stage<3>(bs, bk);
-      best_stage<4>(bs, bk);
-      best_stage<5>(bs, bk);
-      if (bk == NO_KEY) break;   // fewer than k candidates
-      if (lane == r) {
-        rs = bs;
-        rk = bk;
+      for (int r = 0; r < k; ++r) {
+        double bs = hs;
+        int bk = hk;
+        wave_best(bs, bk);
+        if (bk == NO_KEY) break;   // fewer than k candidates
+        if (lane == r) {
+          rs = bs;
+          rk = bk;
+        }
+        nfull = r + 1;
+        if (hk == bk) {            // the winner's lane advances
+          if (is_list) ++hp;
+          else noop_left = false;
+          head();
+        }
       }
-      nfull = r + 1;
-      if (hk == bk) {            // the winner's lane advances
-        if (is_list) ++hp;
-        else noop_left = false;
-        head();
-      }
-    }
-    // Heuristics H (Sec. 4) on B' in rank order: drop x if
-    // score(x) < best - delta, best = B'[0] (possibly terminated, App. A.3);
-    // drop an expansion whose parent already has M kept expansions (no-ops
-    // exempt). A parent's kept expansions before rank r are its first M
-    // delta-survivors, so the M test needs only their count.
-    const double ref = __longlong_as_double(((long long)__builtin_amdgcn_readlane((int)(__double_as_longlong(rs) >> 32), 0) << 32) |
-                                            (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(rs), 0));
-    const int rpar = rk >> 24, rtok = (rk & 0xFFFFFF) - 1;
-    const bool keepd = lane < nfull && !(rs < ref - st.delta);
-    int before = 0;
+      // Heuristics H (Sec. 4) on B' in rank order: drop x if
+      // score(x) < best - delta, best = B'[0] (possibly terminated,
+      // App. A.3); drop an expansion whose parent already has M kept
+      // expansions (no-ops exempt). A parent's kept expansions before rank r
+      // are its first M delta-survivors, so the M test needs only their count.
+      const double ref = __longlong_as_double(((long long)__builtin_amdgcn_readlane((int)(__double_as_longlong(rs) >> 32), 0) << 32) |
+                                              (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(rs), 0));
+      const int rpar = rk >> 24, rtok = (rk & 0xFFFFFF) - 1;
+      const bool keepd = lane < nfull && !(rs < ref - st.delta);
+      int before = 0;
 #pragma unroll 1
-    for (int o = 0; o < nfull; ++o) {
-      const int okk = __builtin_amdgcn_readlane(rk, o);
-      const int okeep = __builtin_amdgcn_readlane((int)keepd, o);
-      before += (o < lane && okeep && (okk >> 24) == rpar && (okk & 0xFFFFFF) != 0);
-    }
-    const bool kept = keepd && (rtok < 0 || before < st.M);
-    int status = SLOT_EMPTY;
-    if (kept) {
-      if (rtok < 0) status = sl_status[rpar];                   // no-op keeps EOS / MAXLEN
-      else status = rtok == 0 ? SLOT_EOS : (t == max_len ? SLOT_MAXLEN : SLOT_ACTIVE);
-    }
-    const unsigned long long km = __ballot(kept);
-    const unsigned long long am = __ballot(kept && status == SLOT_ACTIVE);
-    if (kept) {
-      const int nr = __popcll(km & ((1ull << lane) - 1ull));
-      nscore[nr] = rs;
-      npar[nr] = rpar;
-      ntok[nr] = rtok;
-      nstat[nr] = status;
-    }
-    if (lane == 0) {
-      nw_sh = __popcll(km);
-      nact_sh = __popcll(am);
+      for (int o = 0; o < nfull; ++o) {
+        const int okk = __builtin_amdgcn_readlane(rk, o);
+        const int okeep = __builtin_amdgcn_readlane((int)keepd, o);
+        before += (o < lane && okeep && (okk >> 24) == rpar && (okk & 0xFFFFFF) != 0);
+      }
+      const bool kept = keepd && (rtok < 0 || before < st.M);
+      int status = SLOT_EMPTY;
+      if (kept) {
+        if (rtok < 0) status = sl_status[rpar];                   // no-op keeps EOS / MAXLEN
+        else status = rtok == 0 ? SLOT_EOS : (t == max_len ? SLOT_MAXLEN : SLOT_ACTIVE);
+      }
+      const unsigned long long km = __ballot(kept);
+      const unsigned long long am = __ballot(kept && status == SLOT_ACTIVE);
+      if (kept) {
+        const int nr = __popcll(km & ((1ull << lane) - 1ull));
+        nscore[nr] = rs;
+        npar[nr] = rpar;
+        ntok[nr] = rtok;
+        nstat[nr] = status;
+      }
+      if (lane == 0) {
+        nw_sh = __popcll(km);
+        nact_sh = __popcll(am);
+        no_sh = 0;
+      }
+    } else {
+      // Fairseq rule (App. A.1): a terminated expansion among the best k is
+      // output at once (until k outputs); the new beam is the first k
+      // active expansions in rank order. Both lie within the first 2k ranks.
+      int nact = 0;
+#pragma unroll 1
+      for (int r = 0; r < 2 * k; ++r) {
+        double bs = hs;
+        int bk = hk;
+        wave_best(bs, bk);
+        if (bk == NO_KEY) break;
+        if (lane == r) {
+          rs = bs;
+          rk = bk;
+        }
+        nfull = r + 1;
+        const int wtok = (bk & 0xFFFFFF) - 1;
+        nact += !(wtok == 0 || t == max_len);
+        if (hk == bk) {
+          ++hp;
+          head();
+        }
+        if (nfull >= k && nact >= k) break;
+      }
+      const int rpar = rk >> 24, rtok = (rk & 0xFFFFFF) - 1;
+      const bool valid = lane < nfull;
+      const bool term = valid && (rtok == 0 || t == max_len);
+      const unsigned long long below = (1ull << lane) - 1ull;
+      const unsigned long long tm = __ballot(term && lane < k);
+      const int f = __popcll(tm & below);
+      const bool out = term && lane < k && nout0 + f < k;
+      const unsigned long long act = __ballot(valid && !term);
+      const int nr = __popcll(act & below);
+      const bool inbeam = valid && !term && nr < k;
+      if (out) {
+        oscore[f] = rs;
+        opar[f] = rpar;
+        otok[f] = rtok;
+        ostat[f] = rtok == 0 ? SLOT_EOS : SLOT_MAXLEN;
+      }
+      if (inbeam) {
+        nscore[nr] = rs;
+        npar[nr] = rpar;
+        ntok[nr] = rtok;
+        nstat[nr] = SLOT_ACTIVE;
+      }
+      if (lane == 0) {
+        const int nw = min(k, __popcll(act));
+        const int no = min(__popcll(tm), k - nout0);
+        nw_sh = nw;
+        no_sh = no;
+        // The input finishes with k outputs, or when nothing active is left.
+        nact_sh = (nout0 + no >= k) ? 0 : nw;
+      }
     }
   }
   __syncthreads();
-  const int w = nw_sh;
+  const int w = nw_sh, no = no_sh;
   const bool ends = nact_sh == 0;
+  const int fin = ends ? (int)st.ctrl->timesteps : 0;
 
-  // History: backpointers of level t, indexed by the input's queue position.
-  if (tid < w) {
+  // History: backpointers of level t, indexed by the input's queue position:
+  // the new beam at positions 0..w-1, this step's outputs at k + f.
+  uint32_t *bprow = st.bp + ((size_t)q_in * st.max_len_cap + (t - 1)) * st.bpw;
+  if (tid < w && !(fairseq && ends)) {
     const uint32_t tokbits = ntok[tid] < 0 ? BP_NOOP : (uint32_t)ntok[tid];
-    st.bp[((size_t)q_in * st.max_len_cap + (t - 1)) * k + tid] = ((uint32_t)npar[tid] << 24) | tokbits;
+    bprow[tid] = ((uint32_t)npar[tid] << 24) | tokbits;
+  }
+  if (fairseq && tid >= 64 && tid < 64 + no) {
+    const int f = tid - 64;
+    bprow[k + f] = ((uint32_t)opar[f] << 24) | (uint32_t)otok[f];
+    OutHyp h;
+    h.score = oscore[f];
+    h.length = 0;
+    h.status = ostat[f];
+    h.finalize_step = fin;
+    h.level = t;
+    h.pos = k + f;
+    h.pad = 0;
+    st.o_hyp[(size_t)q_in * k + nout0 + f] = h;
   }
 
   if (ends) {
-    // Y[i] = the survivors in rank order; tokens are rebuilt later.
-    const int fin = (int)st.ctrl->timesteps;
-    if (tid < w) {
-      OutHyp h;
-      h.score = nscore[tid];
-      h.length = 0;
-      h.status = nstat[tid];
-      h.finalize_step = fin;
-      h.level = t;
-      st.o_hyp[(size_t)q_in * k + tid] = h;
+    int total;
+    if (!fairseq) {
+      // Y[i] = the survivors in rank order; tokens are rebuilt later.
+      total = w;
+      if (tid < w) {
+        OutHyp h;
+        h.score = nscore[tid];
+        h.length = 0;
+        h.status = nstat[tid];
+        h.finalize_step = fin;
+        h.level = t;
+        h.pos = tid;
+        h.pad = 0;
+        st.o_hyp[(size_t)q_in * k + tid] = h;
+      }
+    } else {
+      // Y[i] = the outputs in the order they were finalized; those of
+      // earlier steps get the finishing timestep too.
+      total = nout0 + no;
+      if (tid >= 128 && tid < 128 + nout0) st.o_hyp[(size_t)q_in * k + (tid - 128)].finalize_step = fin;
     }
     if (tid < k) {
       st.s_status[base + tid] = SLOT_EMPTY;
       st.s_prow[base + tid] = -1;
     }
     if (tid == 0) {
-      st.o_count[q_in] = w;
+      st.o_count[q_in] = total;
       st.b_input[b] = -1;
-      atomicAdd(reinterpret_cast<unsigned long long *>(&st.ctrl->hyps), (unsigned long long)w);
+      atomicAdd(reinterpret_cast<unsigned long long *>(&st.ctrl->hyps), (unsigned long long)total);
       atomicAdd(reinterpret_cast<unsigned long long *>(&st.ctrl->finished), 1ull);
     }
     return;
@@ -359,6 +453,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   if (tid == 0) {
     st.b_steps[b] = t;
     st.b_par[b] ^= 1;
+    st.b_nout[b] = nout0 + no;
   }
   // State copy: s_h[rank] <- hbuf[row(parent)] for every active survivor,
   // flattened over (survivor, 16-byte chunk) so all threads stream.
@@ -383,19 +478,21 @@ __global__ __launch_bounds__(256) void k_backtrack(DevState st, int q0, int q1) 
   if (q >= q1) return;
   if (rank >= st.o_count[q]) return;
   OutHyp *h = st.o_hyp + (size_t)q * k + rank;
-  const uint32_t *bp = st.bp + (size_t)q * st.max_len_cap * k;
+  const int bpw = st.bpw;
+  const uint32_t *bp = st.bp + (size_t)q * st.max_len_cap * bpw;
   const int top = min(h->level, st.max_len_cap);
-  int pos = rank, len = 0;
+  const int pos0 = min(max(h->pos, 0), bpw - 1);
+  int pos = pos0, len = 0;
   for (int lev = top; lev >= 1; --lev) {
-    const uint32_t e = bp[(size_t)(lev - 1) * k + pos];
+    const uint32_t e = bp[(size_t)(lev - 1) * bpw + pos];
     len += (e & 0xFFFFFFu) != BP_NOOP;
     pos = min((int)(e >> 24), k - 1);
   }
   int32_t *out = st.o_tok + ((size_t)q * k + rank) * st.max_len_cap;
-  pos = rank;
+  pos = pos0;
   int idx = len;
   for (int lev = top; lev >= 1; --lev) {
-    const uint32_t e = bp[(size_t)(lev - 1) * k + pos];
+    const uint32_t e = bp[(size_t)(lev - 1) * bpw + pos];
     const uint32_t tok = e & 0xFFFFFFu;
     if (tok != BP_NOOP) out[--idx] = (int32_t)tok;
     pos = min((int)(e >> 24), k - 1);

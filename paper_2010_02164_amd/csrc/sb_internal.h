@@ -34,6 +34,8 @@ struct DevCtrl {
 struct OutHyp {
   double score;
   int32_t length, status, finalize_step, level;
+  int32_t pos;         // its backpointer entry at `level` (position in that row)
+  int32_t pad;
 };
 
 // All device pointers and sizes a kernel may need, passed by value.
@@ -48,6 +50,7 @@ struct DevState {
   int32_t *b_sel;      // 1 if expanded this step
   int32_t *b_par;      // which KV buffer holds this beam's state
   int32_t *b_ml;       // max_len of the beam's input
+  int32_t *b_nout;     // outputs already finalized (Fairseq rule)
   // candidate slots [n*k], slot = beam*k + rank
   int32_t *s_status;
   double *s_score;
@@ -55,7 +58,7 @@ struct DevState {
   void *s_h;           // [n*k][d] state after consuming the candidate's tokens
   int32_t *s_row;      // row of the slot this step, -1 if not expanded
   int32_t *s_prow;     // for the KV gather: row of the new candidate's parent, -1 if none
-  uint32_t *bp;        // [max_inputs][max_len_cap][k] backpointers, by queue position
+  uint32_t *bp;        // [max_inputs][max_len_cap][bpw] backpointers, by queue position
   // rows [R_max]: per-row metadata written by the scheduler
   int32_t *r_slot;     // slot of the expanded candidate
   int32_t *r_hsrc;     // state source: >= 0 slot index into s_h, < 0 queue row (-1 - q) of q_h0
@@ -87,6 +90,8 @@ struct DevState {
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   int32_t n_cu;        // compute units of the device (persistent launches)
   int32_t select_all;  // 1: expand every live beam (Var-Str-FIFO), 0: minimal l_t only
+  int32_t rule;        // finalization rule: 0 paper (App. A.1), 1 Fairseq
+  int32_t bpw;         // backpointer entries per level: k (paper), 2k (Fairseq: beam + outputs)
   double delta;
   float beta;
 };

@@ -131,6 +131,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
           st.b_steps[b] = 0;
           st.b_par[b] = 0;
           st.b_ml[b] = st.q_ml[inp[u]];
+          st.b_nout[b] = 0;
           for (int j = 0; j < k; ++j) {
             st.s_status[b * k + j] = j == 0 ? SLOT_ACTIVE : SLOT_EMPTY;
             st.s_score[b * k + j] = 0.0;
@@ -228,6 +229,7 @@ __global__ void k_init(DevState st) {
     st.b_steps[i] = 0;
     st.b_sel[i] = 0;
     st.b_par[i] = 0;
+    st.b_nout[i] = 0;
   }
   if (i < st.n * st.k) {
     st.s_status[i] = SLOT_EMPTY;

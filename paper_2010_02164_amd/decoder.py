@@ -39,11 +39,17 @@ def _check(status: int, where: str, dec_handle=None):
     raise N.StreambeamError(status, where, detail)
 
 
-def make_params(k, n, eps, delta, M, sched, max_len_cap, max_inputs) -> N.SbParams:
+def make_params(k, n, eps, delta, M, sched, max_len_cap, max_inputs, rule=None) -> N.SbParams:
+    """sched: a scheduler name (N.SCHEDULERS, or N.FAIRSEQ_SCHEDULERS, which
+    also select the Fairseq finalization rule) or an sb_sched value."""
+    if isinstance(sched, str) and sched in N.FAIRSEQ_SCHEDULERS:
+        code, rule = N.FAIRSEQ_SCHEDULERS[sched], N.SB_RULE_FAIRSEQ
+    else:
+        code = N.SCHEDULERS[sched] if isinstance(sched, str) else int(sched)
     return N.SbParams(k=int(k), n=int(n), eps=float(eps),
                       delta=float(math.inf if delta is None else delta), max_per_node=int(M),
-                      sched=N.SCHEDULERS[sched] if isinstance(sched, str) else int(sched),
-                      max_len_cap=int(max_len_cap), max_inputs=int(max_inputs))
+                      sched=code, max_len_cap=int(max_len_cap), max_inputs=int(max_inputs),
+                      finalize_rule=int(N.SB_RULE_PAPER if rule is None else rule))
 
 
 def make_model(vocab, d, dtype, beta, W_h=0, E=0, W_out=0, kv_layers=0, W_kv=0) -> N.SbModel:

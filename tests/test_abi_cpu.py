@@ -45,11 +45,21 @@ def test_workspace_sizes(native_lib, i):
     (dict(sched=7), N.SB_E_INVALID_ARG), (dict(max_len_cap=0), N.SB_E_INVALID_ARG),
     (dict(max_inputs=0), N.SB_E_INVALID_ARG), (dict(vocab=3), N.SB_E_INVALID_ARG),
     (dict(n=0), N.SB_E_UNSUPPORTED), (dict(kv_layers=2), N.SB_E_UNSUPPORTED),
+    (dict(finalize_rule=2), N.SB_E_INVALID_ARG), (dict(k=16, finalize_rule=1), N.SB_E_UNSUPPORTED),
 ])
 def test_validate_rejects(native_lib, over, code):
     m, p = _mp(CONFIGS[3], **over)
     assert native_lib.sb_validate(ctypes.byref(m), ctypes.byref(p)) == code
     assert workspace_bytes(m, p) == 0
+
+
+def test_fairseq_rule_workspace(native_lib):
+    # The Fairseq rule keeps 2k backpointers per level (beam + outputs).
+    m, p = _mp(CONFIGS[3])
+    m2, p2 = _mp(CONFIGS[3], finalize_rule=1)
+    c = CONFIGS[3]
+    assert native_lib.sb_validate(ctypes.byref(m2), ctypes.byref(p2)) == N.SB_OK
+    assert workspace_bytes(m2, p2) >= workspace_bytes(m, p) + c.N * c.max_len_cap * c.k * 4
 
 
 def test_delta_inf_is_valid(native_lib):

@@ -1,5 +1,6 @@
-"""End-to-end parity of the HIP search with the oracle (Fixed, Var-Batch,
-Var-Stream, Var-Str-FIFO), batch invariance and determinism."""
+"""End-to-end parity of the HIP search with the oracle (Fixed, Fixed-Stream,
+Fixed-Fairseq, Var-Batch, Var-Stream, Var-Str-FIFO), batch invariance and
+determinism."""
 import numpy as np
 import pytest
 
@@ -8,7 +9,8 @@ from tests.gpu_util import check_parity, gpu_decode
 
 pytestmark = pytest.mark.gpu
 
-SCHEDS = ["fixed", "var_batch", "var_stream", "var_fifo"]
+SCHEDS = ["fixed", "var_batch", "var_stream", "var_fifo", "fixed_stream", "fixed_fairseq",
+          "fixed_fairseq_stream"]
 
 
 @pytest.mark.parametrize("sched", SCHEDS)
@@ -23,7 +25,7 @@ def test_cfg2_reduced(gpu, sched):
     check_parity(wl, sched)
 
 
-@pytest.mark.parametrize("sched", ["var_batch", "var_stream", "var_fifo"])
+@pytest.mark.parametrize("sched", ["var_batch", "var_stream", "var_fifo", "fixed_fairseq_stream"])
 def test_cfg3_reduced(gpu, sched):
     wl = make_workload(scaled(3, N=40, n=16, V=8000))
     check_parity(wl, sched)
@@ -44,6 +46,17 @@ def test_stream_equals_batch_on_gpu_bitwise(gpu):
         assert key == [(h.tokens, h.score, h.status) for h in yc]
         assert key == [(h.tokens, h.score, h.status) for h in yf]
     assert sa["expansions"] == sb["expansions"] == sf["expansions"]
+
+
+def test_fairseq_rule_stream_equals_batch_on_gpu_bitwise(gpu):
+    # The Fairseq finalization rule with and without the streaming refill.
+    wl = make_workload(scaled(1, N=64))
+    a, sa, _ = gpu_decode(wl, "fixed_fairseq")
+    b, sb, _ = gpu_decode(wl, "fixed_fairseq_stream", eps=0.5, n=6)
+    for ya, yb in zip(a, b):
+        assert len(ya) == wl.cfg.k
+        assert [(h.tokens, h.score, h.status) for h in ya] == [(h.tokens, h.score, h.status) for h in yb]
+    assert sa["expansions"] == sb["expansions"] and sa["noops"] == 0
 
 
 def test_deterministic(gpu):
