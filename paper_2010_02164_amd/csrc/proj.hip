@@ -33,13 +33,13 @@ constexpr int CH = 128;          // bytes of a row's K chunk
 constexpr int LS = CH + 16;      // padded LDS row stride (bytes)
 constexpr int FRAG = 1024;       // bytes of one wave-wide 16-byte-per-lane fragment
 constexpr int WCH = 4 * FRAG;    // bytes of one wave's W_out fragments per chunk
-constexpr int D = 3;             // prefetch depth (chunks)
 
 template <int KB>
 union ProjSmem {
-  unsigned char B[2][2][TR][LS];          // [buffer][K half][row][byte]
+  unsigned char B[2][2][TR][LS];          // [buffer][wave group][row][byte]
   float red[2][4][2][16][64];             // [sending half][slice][block][reg][lane]
   float xch[4][TR][part_width(KB)];       // [slice][row][max, sumexp, keys]
+  float xr[2][2][4][32][part_width(KB)];  // [buffer][group][slice][row][...], one block at a time
 };
 
 // K loop of one wave over its half: acc[b] (b < NBV) += W_out fragment x
@@ -47,7 +47,7 @@ union ProjSmem {
 // (+ lane * 16 + q * 1 KB), the half's state tile at bbase + c * 128 bytes
 // (+ boff[u]). Loads of a chunk are issued together, D chunks ahead of use,
 // at indices clamped to the last chunk so that no load sits in a branch.
-template <bool BF16, int NBV>
+template <bool BF16, int NBV, int D>
 __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned char (*Bt1)[LS],
                                               const unsigned char *abase, uint32_t alane,
                                               const unsigned char *bbase, const uint32_t *boff, int srow,
@@ -125,12 +125,85 @@ __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned 
   }
 }
 
-// One 128 x 128 output tile (vocabulary tile vt, batch tile rt).
+// Lane-level epilogue of one 32-row block: lane holds batch row l32 of the
+// block and the wave's vocabulary rows v0 + 32wv + 8*(reg/4) + 4h + reg%4
+// (increasing with reg). Adds the EOS bias, folds the 16 logits into
+// (max, sum exp) and a sorted best-KB key list, then combines lanes l and
+// l+32 (same row), which end with identical results.
+template <int KB>
+__device__ __forceinline__ void block_lists(const f16v &z, int v0, int wv, int h, int V, float bias, float &m_out,
+                                            float &s_out, TopK<KB> &tk) {
+  float vals[16];
+#pragma unroll
+  for (int reg = 0; reg < 16; ++reg) {
+    const int v = v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3);
+    const float zz = v == 0 ? z[reg] + bias : z[reg];
+    vals[reg] = v < V ? zz : -INFINITY;
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) m = fmaxf(m, vals[q]);
+  float s = 0.0f;
+  if (m > -INFINITY) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) s += __expf(vals[q] - m);
+  }
+  // The lane's 16 candidates as ranking keys, sorted by a network.
+  cand_key keys[16];
+#pragma unroll
+  for (int reg = 0; reg < 16; ++reg) keys[reg] = make_key(vals[reg], v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3));
+  bitonic_sort_desc<16>(keys);
+  TopK<KB> lo, hi;
+#pragma unroll
+  for (int q = 0; q < KB; ++q) stage64<5>(keys[q], lo.k[q], hi.k[q]);
+  topk_merge(lo, hi);
+  tk = lo;
+  uint32_t ma, mb, sa, sb;
+  stage32<5>(__float_as_uint(m), ma, mb);
+  stage32<5>(__float_as_uint(s), sa, sb);
+  m = __uint_as_float(ma);
+  s = __uint_as_float(sa);
+  lse_merge(m, s, __uint_as_float(mb), __uint_as_float(sb));
+  m_out = m;
+  s_out = s;
+}
+
+// Partial record of (row j, vocabulary tile vt): the merge of the four
+// vocabulary slices' (max, sum exp, key list), read from LDS.
+template <int KB>
+__device__ __forceinline__ void write_record(const DevState &st, int j, int vt, const float *const *slices) {
+  constexpr int PW = part_width(KB);
+  float m = -INFINITY, s = 0.0f;
+  TopK<KB> tk;
+  topk_init(tk);
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+    const float *p = slices[x];
+    TopK<KB> o;
+    topk_load(o, p + 2);
+    lse_merge(m, s, p[0], p[1]);
+    topk_merge(tk, o);
+  }
+  float rec[PW];
+  rec[0] = m;
+  rec[1] = s;
+  topk_store(rec + 2, tk);
+#pragma unroll
+  for (int x = 2 + 2 * KB; x < PW; ++x) rec[x] = 0.0f;
+  u4 *out = reinterpret_cast<u4 *>(st.part + ((size_t)j * st.S + vt) * PW);
+#pragma unroll
+  for (int x = 0; x < PW / 4; ++x)
+    out[x] = u4{__float_as_uint(rec[4 * x]), __float_as_uint(rec[4 * x + 1]), __float_as_uint(rec[4 * x + 2]),
+                __float_as_uint(rec[4 * x + 3])};
+}
+
+// Tile of at most 4 blocks (128 rows from r0): the K range is split in two
+// fixed halves, waves 0-3 summing the first, waves 4-7 the second; the two
+// partial sums are added once.
 template <bool BF16, int KB>
-__device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, int vt, int rt, int R) {
+__device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB> &sm, int vt, int r0, int R, int nbv) {
   const int d = st.d, V = st.V;
-  const int v0 = vt * TV, r0 = rt * TR;
-  const int nbv = min(NB, (R - r0 + 31) >> 5);    // blocks holding valid rows
+  const int v0 = vt * TV;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = w >> 2, wv = w & 3;               // K half, vocabulary slice
@@ -159,10 +232,10 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
   unsigned char (*Bt1)[LS] = sm.B[1][g];
   const uint32_t alane = (uint32_t)lane * 16u;
   switch (nbv) {
-    case 1: proj_mainloop<BF16, 1>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
-    case 2: proj_mainloop<BF16, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
-    case 3: proj_mainloop<BF16, 3>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
-    default: proj_mainloop<BF16, 4>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    case 1: proj_mainloop<BF16, 1, 3>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    case 2: proj_mainloop<BF16, 2, 3>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    case 3: proj_mainloop<BF16, 3, 3>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
+    default: proj_mainloop<BF16, 4, 3>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc); break;
   }
 
   // Combine the halves. Half g owns blocks 2g and 2g+1: it sends its sums of
@@ -190,10 +263,7 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
     }
   }
 
-  // Epilogue on the owned blocks. Block 2g+bl: lane holds batch row
-  // r0 + 32(2g+bl) + l32 and the wave's vocabulary rows
-  // v0 + 32wv + 8*(reg/4) + 4h + reg%4, increasing with reg.
-  constexpr int PW = part_width(KB);
+  // Epilogue on the owned blocks 2g + bl.
   TopK<KB> tks[2];
   float ms[2], ss[2];
 #pragma unroll
@@ -202,45 +272,7 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
     if (blk < nbv) {
       const int j = r0 + 32 * blk + l32;
       const float bias = (v0 == 0 && j < R) ? st.beta * (float)(st.r_t[j] - st.r_Lx[j]) : 0.0f;
-      float vals[16];
-#pragma unroll
-      for (int reg = 0; reg < 16; ++reg) {
-        const int v = v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3);
-        float z = own[bl][reg];
-        if (v == 0) z += bias;
-        vals[reg] = v < V ? z : -INFINITY;
-      }
-      float m = -INFINITY;
-#pragma unroll
-      for (int q = 0; q < 16; ++q) m = fmaxf(m, vals[q]);
-      float s = 0.0f;
-      if (m > -INFINITY) {
-#pragma unroll
-        for (int q = 0; q < 16; ++q) s += __expf(vals[q] - m);
-      }
-      // The lane's 16 candidates as ranking keys, sorted by a network.
-      cand_key keys[16];
-#pragma unroll
-      for (int reg = 0; reg < 16; ++reg)
-        keys[reg] = make_key(vals[reg], v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3));
-      bitonic_sort_desc<16>(keys);
-#pragma unroll
-      for (int q = 0; q < KB; ++q) tks[bl].k[q] = keys[q];
-      // Lanes l and l+32 hold the same row: combine their lists and sums
-      // (both lanes get the same result).
-      TopK<KB> lo, hi;
-#pragma unroll
-      for (int q = 0; q < KB; ++q) stage64<5>(tks[bl].k[q], lo.k[q], hi.k[q]);
-      topk_merge(lo, hi);
-      tks[bl] = lo;
-      uint32_t ma, mb, sa, sb;
-      stage32<5>(__float_as_uint(m), ma, mb);
-      stage32<5>(__float_as_uint(s), sa, sb);
-      m = __uint_as_float(ma);
-      s = __uint_as_float(sa);
-      lse_merge(m, s, __uint_as_float(mb), __uint_as_float(sb));
-      ms[bl] = m;
-      ss[bl] = s;
+      block_lists<KB>(own[bl], v0, wv, h, V, bias, ms[bl], ss[bl], tks[bl]);
     }
   }
   __syncthreads();   // the exchange area is reused below
@@ -260,30 +292,134 @@ __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, 
     const int row = 32 * w + l32;
     const int j = r0 + row;
     if (j < R) {
-      float m = -INFINITY, s = 0.0f;
-      TopK<KB> tk;
-      topk_init(tk);
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const float *p = sm.xch[x][row];
-        TopK<KB> o;
-        topk_load(o, p + 2);
-        lse_merge(m, s, p[0], p[1]);
-        topk_merge(tk, o);
-      }
-      float rec[PW];
-      rec[0] = m;
-      rec[1] = s;
-      topk_store(rec + 2, tk);
-#pragma unroll
-      for (int x = 2 + 2 * KB; x < PW; ++x) rec[x] = 0.0f;
-      u4 *out = reinterpret_cast<u4 *>(st.part + ((size_t)j * st.S + vt) * PW);
-#pragma unroll
-      for (int x = 0; x < PW / 4; ++x)
-        out[x] = u4{__float_as_uint(rec[4 * x]), __float_as_uint(rec[4 * x + 1]), __float_as_uint(rec[4 * x + 2]),
-                    __float_as_uint(rec[4 * x + 3])};
+      const float *sl[4] = {sm.xch[0][row], sm.xch[1][row], sm.xch[2][row], sm.xch[3][row]};
+      write_record<KB>(st, j, vt, sl);
     }
   }
+}
+
+// Tile of 5 to 8 blocks (rows r0 .. r0+255): the blocks are split between
+// the two wave groups (nbh each, the last block possibly padding), and every
+// wave sums its blocks over the first K half and then over the second, in
+// two accumulators added once at the end: the same order of additions as a
+// K-split tile, so a row's logits do not depend on how the step was tiled.
+template <bool BF16, int KB>
+__device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &sm, int vt, int r0, int R, int nbt) {
+  const int d = st.d, V = st.V;
+  const int v0 = vt * TV;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = w >> 2, wv = w & 3;               // row group, vocabulary slice
+  const int l32 = lane & 31, h = lane >> 5;
+  const int rowbytes = d * (BF16 ? 2 : 4);
+  const int nk = rowbytes / CH;
+  const int nh = nk >> 1;
+  const int nbh = (nbt + 1) >> 1;                 // blocks per group (3 or 4)
+  const int gb0 = g * nbh;                        // first block of this group
+
+  const int tg = tid & 255;
+  const int srow = tg >> 3, scol = (tg & 7) * 16;
+  uint32_t boff[NB];
+#pragma unroll
+  for (int u = 0; u < NB; ++u)
+    boff[u] = (uint32_t)min(r0 + 32 * (gb0 + u) + srow, R - 1) * (uint32_t)rowbytes + scol;
+  unsigned char (*Bt)[LS] = sm.B[0][g];
+  unsigned char (*Bt1)[LS] = sm.B[1][g];
+  const uint32_t alane = (uint32_t)lane * 16u;
+  const unsigned char *hb = static_cast<const unsigned char *>(st.hbuf);
+  f16v acc0[NB], acc1[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    acc0[b] = f16v{};
+    acc1[b] = f16v{};
+  }
+  // The two K halves in turn, each into its own accumulators.
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int kbeg = half * nh;
+    const unsigned char *abase = st.wout_t + ((size_t)(vt * nk + kbeg) * 4 + wv) * WCH;
+    const unsigned char *bbase = hb + (size_t)kbeg * CH;
+    f16v *acc = half ? acc1 : acc0;
+    if (half) __syncthreads();   // the staging tile of the first half is done
+    if (nbh == 3)
+      proj_mainloop<BF16, 3, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
+    else
+      proj_mainloop<BF16, 4, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
+  }
+
+  // Epilogue, one owned block at a time: lane lists, then wave i of the
+  // group merges block i's four vocabulary slices (double-buffered LDS).
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    if (i < nbh) {
+      const int blk = gb0 + i;
+      const int buf = i & 1;
+      if (blk < nbt) {
+        f16v z;
+#pragma unroll
+        for (int reg = 0; reg < 16; ++reg) z[reg] = acc0[i][reg] + acc1[i][reg];
+        const int j = r0 + 32 * blk + l32;
+        const float bias = (v0 == 0 && j < R) ? st.beta * (float)(st.r_t[j] - st.r_Lx[j]) : 0.0f;
+        float m, s;
+        TopK<KB> tk;
+        block_lists<KB>(z, v0, wv, h, V, bias, m, s, tk);
+        if (lane < 32) {
+          float *p = sm.xr[buf][g][wv][l32];
+          p[0] = m;
+          p[1] = s;
+          topk_store(p + 2, tk);
+        }
+      }
+      __syncthreads();
+      if (blk < nbt && wv == i && lane < 32) {
+        const int j = r0 + 32 * blk + l32;
+        if (j < R) {
+          const float *sl[4] = {sm.xr[buf][g][0][l32], sm.xr[buf][g][1][l32], sm.xr[buf][g][2][l32],
+                                sm.xr[buf][g][3][l32]};
+          write_record<KB>(st, j, vt, sl);
+        }
+      }
+    }
+  }
+}
+
+// Row tile rt covers blocks bt*rt .. bt*rt + bt - 1 (32 rows each) of
+// vocabulary tile vt.
+template <bool BF16, int KB>
+__device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, int vt, int rt, int R, int bt) {
+  const int r0 = rt * bt * 32;
+  const int nbt = min(bt, (R - r0 + 31) >> 5);   // blocks holding valid rows
+  if constexpr (BF16) {
+    proj_tile_ksplit<BF16, KB>(st, sm, vt, r0, R, nbt);
+  } else {
+    if (nbt <= NB)
+      proj_tile_ksplit<BF16, KB>(st, sm, vt, r0, R, nbt);
+    else
+      proj_tile_big<BF16, KB>(st, sm, vt, r0, R, nbt);
+  }
+}
+
+// Blocks per row tile for a step of R rows: the count (1..8) that minimizes
+// rounds x tile cost, where a round is one tile per workgroup and a tile
+// costs its MFMA blocks (a big tile computes an even count) plus a fixed
+// part worth 0.7 block (prologue, epilogue). Ties go to the larger tile.
+// The bf16 path keeps 4-block tiles: its MFMA blocks are cheap next to the
+// per-block epilogue, so fewer rounds of larger tiles do not pay there.
+__device__ __forceinline__ int row_tile_blocks(int R, int S, int G) {
+  const int B = (R + 31) >> 5;
+  int best_bt = NB;
+  float best = 3.0e38f;
+  for (int bt = 1; bt <= 2 * NB; ++bt) {
+    const int nra = (B + bt - 1) / bt;
+    const int be = min(bt, B);
+    const int rounds = (S * nra + G - 1) / G;
+    const float cost = (float)rounds * ((float)(be <= NB ? be : 2 * ((be + 1) >> 1)) + 0.7f);
+    if (cost <= best) {
+      best = cost;
+      best_bt = bt;
+    }
+  }
+  return best_bt;
 }
 
 // Persistent launch: at most one workgroup per compute unit, each walking
@@ -300,7 +436,8 @@ template <bool BF16, int KB>
 __global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
   const int R = st.ctrl->R;
   if (R <= 0) return;
-  const int nra = (R + TR - 1) / TR;
+  const int bt = BF16 ? NB : row_tile_blocks(R, st.S, (int)gridDim.x);
+  const int nra = (R + 32 * bt - 1) / (32 * bt);
   const int T = st.S * nra;
   const int x = blockIdx.x & 7, gx = gridDim.x >> 3, j = blockIdx.x >> 3;
   const int lo = (int)((long long)T * x / 8), nt = (int)((long long)T * (x + 1) / 8) - lo;
@@ -310,7 +447,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
     if (idx >= nt) continue;
     const int tile = lo + idx;
     const int vt = tile / nra, rt = tile - vt * nra;
-    proj_tile<BF16, KB>(st, sm, vt, rt, R);
+    proj_tile<BF16, KB>(st, sm, vt, rt, R, bt);
     __syncthreads();   // LDS is reused by the next tile
   }
 }
