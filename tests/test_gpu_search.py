@@ -48,6 +48,23 @@ def test_stream_equals_batch_on_gpu_bitwise(gpu):
     assert sa["expansions"] == sb["expansions"] == sf["expansions"]
 
 
+def test_stream_equals_batch_bitwise_across_row_tilings(gpu):
+    # Steps of up to n*k = 640 rows: the projection picks its row-tile height
+    # per step (32 to 256 rows), so one input's rows meet different tilings
+    # under the three schedules; its logits must not change.
+    wl = make_workload(scaled(3, N=160, n=128, V=8000))
+    a, sa, da = gpu_decode(wl, "var_batch")
+    b, sb, _ = gpu_decode(wl, "var_stream")
+    f, sf, _ = gpu_decode(wl, "var_fifo", n=45)
+    counts, width = da.rows_histogram()
+    assert sum(c for i, c in enumerate(counts) if i * width > 256) > 0   # some steps use 256-row tiles
+    for ya, yb, yf in zip(a, b, f):
+        key = [(h.tokens, h.score, h.status) for h in ya]
+        assert key == [(h.tokens, h.score, h.status) for h in yb]
+        assert key == [(h.tokens, h.score, h.status) for h in yf]
+    assert sa["expansions"] == sb["expansions"] == sf["expansions"]
+
+
 def test_fairseq_rule_stream_equals_batch_on_gpu_bitwise(gpu):
     # The Fairseq finalization rule with and without the streaming refill.
     wl = make_workload(scaled(1, N=64))
