@@ -17,6 +17,13 @@ m = min(n - |B|, inputs left), i.e. it refills the batch to n (Sec. 3: the
 initial batch is n and a refill restores size n); inputs are admitted in
 index order; Var-Batch is eps = 0 (refill only when the batch is empty) and
 Fixed is eps = 0, delta = inf, M = k (App. A.1: Fixed-Ours is eps = 0).
+
+Capacity-constrained streaming (Sec. 3, last paragraph; Sec. 4.2 and 4.3,
+a limit of n*k expanded candidates per timestep): up to `pool` >= n beams
+are cached; the refill test and amount use the pool size in place of n; at
+each timestep the live beams, ordered by (l_t, admission order), are taken
+while their active candidates total at most n*k rows (the first beam that
+would exceed the limit ends the selection).
 """
 from __future__ import annotations
 
@@ -72,7 +79,8 @@ class _Beam:
 def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
            n: int, eps: float, k: int, delta: float = math.inf,
            M: Optional[int] = None, on_step: Optional[Callable] = None,
-           select: str = "min_steps", rule: str = "paper") -> SearchResult:
+           select: str = "min_steps", rule: str = "paper",
+           pool: Optional[int] = None) -> SearchResult:
     """Run Alg. 1 over inputs 0..N-1 (h0[i] is e_i = E(x_i)).
 
     `decoder` needs initial_state(h0_row) and expand(h_prev, y, t, Lx) ->
@@ -81,20 +89,25 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
     schedule. `select` is Alg. 1's beam selection, "min_steps" (the beams
     with minimal l_t), or "fifo" for Var-Str-FIFO (App. A, alternative
     method analysis: beams up to the batch capacity n, starting from the
-    one with maximal l_t). `rule` is the finalization rule: "paper"
+    one with maximal l_t), or "capacity" (the capacity-constrained
+    selection above; `pool` beams are cached, default n). `rule` is the
+    finalization rule: "paper"
     (App. A.1: terminated candidates stay on the beam) or "fairseq"
     (App. A.1's Fixed-Fairseq: they are output at once; fixed width, so
     delta and M are not applied); a beam under the Fairseq rule finishes
     with k outputs, kept in the order they were finalized.
     """
-    if select not in ("min_steps", "fifo"):
+    if select not in ("min_steps", "fifo", "capacity"):
         raise ValueError(select)
     if rule not in ("paper", "fairseq"):
         raise ValueError(rule)
     N = len(Lx)
     M = k if M is None else int(M)
-    if not (k >= 1 and n >= 1 and 0.0 <= eps < 1.0 and 1 <= M <= k):
+    P = n if pool is None else int(pool)
+    if not (k >= 1 and n >= 1 and 0.0 <= eps < 1.0 and 1 <= M <= k and P >= n):
         raise ValueError("invalid search parameters")
+    if P != n and select != "capacity":
+        raise ValueError("a beam pool larger than n needs the capacity selection")
     res = SearchResult(hyps=[None] * N, finalize_step=np.zeros(N, np.int64),
                        steps_taken=np.zeros(N, np.int64),
                        min_margin=np.full(N, np.inf),
@@ -102,8 +115,8 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
     c = 0
     live: List[_Beam] = []
     while c < N or live:
-        if c < N and len(live) <= eps * n:
-            m = min(n - len(live), N - c)
+        if c < N and len(live) <= eps * P:
+            m = min(P - len(live), N - c)
             for i in range(c, c + m):
                 st = decoder.initial_state(h0[i])
                 live.append(_Beam(i, 0, [Cand(0.0, (), ACTIVE, st, 0)]))
@@ -115,6 +128,14 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
             # At most n beams are live, so the capacity-n prefix of the
             # beams ordered by decreasing l_t is every live beam.
             sel = sorted(live, key=lambda b: -b.steps)[:n]
+        elif select == "capacity":
+            sel, used = [], 0
+            for b in sorted(live, key=lambda b: (b.steps, b.input)):
+                width = sum(1 for cand in b.cands if cand.status == ACTIVE)
+                if used + width > n * k:
+                    break
+                sel.append(b)
+                used += width
         else:
             sel = [b for b in live if b.steps == lmin]
 
@@ -172,10 +193,12 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
 
 
 def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var_stream",
-                    inputs: Optional[Sequence[int]] = None, decoder=None) -> SearchResult:
+                    inputs: Optional[Sequence[int]] = None, decoder=None,
+                    pool: Optional[int] = None) -> SearchResult:
     """Convenience wrapper: decode (a subset of) a synthgen Workload with its
     config's parameters; `sched` picks Fixed / Fixed-Stream / Fixed-Fairseq /
-    Var-Batch / Var-Stream / Var-Str-FIFO ("var_fifo")."""
+    Var-Batch / Var-Stream / Var-Str-FIFO ("var_fifo") / capacity-constrained
+    Var-Stream ("var_cap", `pool` cached beams, default 2n)."""
     from .decoder import ElmanDecoder
     c = wl.cfg
     dec = decoder or ElmanDecoder.from_workload(wl)
@@ -195,8 +218,13 @@ def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var
         delta, M, rule = math.inf, k, "fairseq"
     elif sched == "var_batch":
         eps = 0.0
-    elif sched not in ("var_stream", "var_fifo"):
+    elif sched not in ("var_stream", "var_fifo", "var_cap"):
         raise ValueError(sched)
+    select = {"var_fifo": "fifo", "var_cap": "capacity"}.get(sched, "min_steps")
+    if sched == "var_cap":
+        pool = 2 * n if pool is None else pool
+    elif pool is not None:
+        raise ValueError("pool applies to var_cap only")
     idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
     return decode(dec, wl.h0[idx], wl.Lx[idx], wl.max_len[idx], n, eps, k, delta, M,
-                  select="fifo" if sched == "var_fifo" else "min_steps", rule=rule)
+                  select=select, rule=rule, pool=pool)

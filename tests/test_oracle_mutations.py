@@ -48,6 +48,8 @@ PINS = {
     "fairseq": lambda: tsearch.test_scripted_cases(_cases()["fairseq_outputs_terminated_immediately"]),
     "fairseq_exhaustive": lambda: tsearch.test_fairseq_rule_exhaustive(3, 4, 1),
     "fig1": tsearch.test_fig1_schedule,
+    "cap_schedule": tsearch.test_capacity_schedule,
+    "cap_replay": lambda: tsearch.test_capacity_schedule_event_replay(0.25, 12),
     "stream_vs_batch": lambda: tsearch.test_var_stream_matches_var_batch(0, 4, 0.25),
 }
 
@@ -76,7 +78,18 @@ MUTATIONS = [
      "for score, j, w in pool[:2 * k]:", ["fairseq"]),
     ("fairseq_beam_keeps_terminated", "beam", "        if terminated(w):\n            continue\n", "",
      ["fairseq", "fairseq_exhaustive"]),
-    ("refill_strict", "search", "len(live) <= eps * n", "len(live) < eps * n", ["fig1"]),
+    ("refill_strict", "search", "len(live) <= eps * P", "len(live) < eps * P", ["fig1", "cap_schedule"]),
+    ("refill_against_n", "search", "len(live) <= eps * P", "len(live) <= eps * n", ["cap_schedule"]),
+    ("refill_to_n", "search", "m = min(P - len(live), N - c)", "m = min(n - len(live), N - c)",
+     ["cap_schedule"]),
+    ("capacity_longest_first", "search", "key=lambda b: (b.steps, b.input)",
+     "key=lambda b: (-b.steps, b.input)", ["cap_schedule"]),
+    ("capacity_ties_reversed", "search", "key=lambda b: (b.steps, b.input)",
+     "key=lambda b: (b.steps, -b.input)", ["cap_schedule"]),
+    ("capacity_limit_of_pool", "search", "if used + width > n * k:", "if used + width > P * k:",
+     ["cap_schedule"]),
+    ("capacity_skips_instead_of_stopping", "search", "                    break\n                sel.append(b)",
+     "                    continue\n                sel.append(b)", ["cap_replay"]),
     ("expand_all_live", "search", "sel = [b for b in live if b.steps == lmin]", "sel = list(live)", ["fig1"]),
     ("bias_uses_global_timestep", "search", "t = np.array([sel[bi].steps + 1 for bi, _ in rows])",
      "t = np.array([res.timesteps + 1 for bi, _ in rows])", ["stream_vs_batch", "greedy"]),

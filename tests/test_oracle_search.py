@@ -208,19 +208,30 @@ def test_fixed_stream_matches_fixed():
     assert a.expansions == b.expansions
 
 
-def _replay(widths, n, eps, fifo=False):
+def _replay(widths, n, eps, fifo=False, pool=None, budget=None):
     """Independent event simulation of Alg. 1's schedule from each input's
     per-step active widths: returns (rows per timestep, finalize timesteps).
-    fifo: every live beam steps (Var-Str-FIFO); else the minimal-l_t ones."""
+    fifo: every live beam steps (Var-Str-FIFO); pool/budget: up to `pool`
+    beams cached, and beams step in (l_t, input) order while their widths
+    fit in `budget` rows; else the minimal-l_t ones."""
     N = len(widths)
+    P = pool or n
     c, live, rows, fin = 0, [], [], [0] * N
     while c < N or live:
-        if c < N and len(live) <= eps * n:
-            m = min(n - len(live), N - c)
+        if c < N and len(live) <= eps * P:
+            m = min(P - len(live), N - c)
             live += [[i, 0] for i in range(c, c + m)]
             c += m
         lo = min(s for _, s in live)
-        sel = list(live) if fifo else [b for b in live if b[1] == lo]
+        if budget is not None:
+            sel, used = [], 0
+            for b in sorted(live, key=lambda b: (b[1], b[0])):
+                if used + widths[b[0]][b[1]] > budget:
+                    break
+                used += widths[b[0]][b[1]]
+                sel.append(b)
+        else:
+            sel = list(live) if fifo else [b for b in live if b[1] == lo]
         rows.append(sum(widths[i][s] for i, s in sel))
         for b in sel:
             b[1] += 1
@@ -246,6 +257,53 @@ def test_fifo_schedule_event_replay(eps):
     rows, fin = _replay(res.widths, 6, eps, fifo=True)
     assert rows == res.rows_per_step
     assert fin == list(res.finalize_step)
+
+
+@pytest.mark.parametrize("eps,pool", [(0.25, 12), (0.5, 9), (0.0, 18)])
+def test_capacity_schedule_event_replay(eps, pool):
+    # Variable widths (delta and M pruning) make the row limit bind at
+    # different beams from step to step.
+    cfg = scaled(1, N=30, V=50, d=12, len_hi=12, seed=7100, delta=1.2, M=3, k=4)
+    wl = make_workload(cfg)
+    res = decode_workload(wl, n=6, eps=eps, sched="var_cap", pool=pool)
+    rows, fin = _replay(res.widths, 6, eps, pool=pool, budget=6 * cfg.k)
+    assert rows == res.rows_per_step
+    assert fin == list(res.finalize_step)
+    assert max(res.rows_per_step) <= 6 * cfg.k
+    assert len(set(w for ws in res.widths for w in ws)) > 2
+
+
+@pytest.mark.parametrize("cfg_seed,n,eps", [(0, 4, 0.25), (2, 3, 1 / 3), (3, 8, 0.5)])
+def test_capacity_pool_of_n_is_fifo(cfg_seed, n, eps):
+    # With no more beams cached than n, every live beam fits the n k row
+    # limit, so the capacity-constrained selection takes them all: the
+    # schedule is Var-Str-FIFO's step for step (App. A), and outputs are
+    # Var-Batch's (Sec. 3) for any pool size.
+    cfg = scaled(1, N=21, V=60, d=12, len_hi=9, seed=7000 + cfg_seed, delta=1.2, M=3, k=4)
+    wl = make_workload(cfg)
+    vf = decode_workload(wl, n=n, eps=eps, sched="var_fifo")
+    vc = decode_workload(wl, n=n, eps=eps, sched="var_cap", pool=n)
+    assert vc.rows_per_step == vf.rows_per_step
+    assert list(vc.finalize_step) == list(vf.finalize_step)
+    vb = decode_workload(wl, n=n, sched="var_batch")
+    for pool in (n, 2 * n, 3 * n + 1):
+        v = decode_workload(wl, n=n, eps=eps, sched="var_cap", pool=pool)
+        _same_outputs(vb, v)
+        assert v.expansions == vb.expansions and v.noops == vb.noops
+        assert max(v.rows_per_step) <= n * cfg.k
+
+
+def test_capacity_schedule():
+    with open(os.path.join(GOLDEN, "capacity_schedule.json")) as f:
+        g = json.load(f)
+    L = g["L"]
+    trace = []
+    res = decode(LengthDecoder(g["V"]), np.zeros((len(L), 1)), L, [50] * len(L), n=g["n"],
+                 eps=g["eps"], k=g["k"], on_step=lambda t, sel, r: trace.append([t, sorted(sel)]),
+                 select="capacity", pool=g["pool"])
+    assert trace == g["trace"]
+    assert res.rows_per_step == g["rows_per_step"]
+    assert list(res.finalize_step) == g["finalize_step"]
 
 
 def test_fig1_schedule():
