@@ -41,14 +41,15 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_proj_traffic.md")
 METRIC = "finalized hyps/sec + expansions/sec (Var-Stream, k=5, |V|=32k), % roofline"
 
 
-def _workload_desc(cfg, sched, eps):
+def _workload_desc(cfg, sched, eps, pool=None):
     return (f"{cfg.name}: N={cfg.N} inputs, n={cfg.n}, k={cfg.k}, |V|={cfg.V}, d={cfg.d}, "
-            f"{cfg.dtype}, {sched} eps={eps:g}, delta={cfg.delta:g}, M={cfg.M}, "
+            f"{cfg.dtype}, {sched} eps={eps:g}" + (f" pool={pool}" if pool else "")
+            + f", delta={cfg.delta:g}, M={cfg.M}, "
             f"L_x {cfg.lengths}[{cfg.len_lo},{cfg.len_hi}]"
             + (f", KV {cfg.kv_layers}x2xtxd" if cfg.kv_layers else ""))
 
 
-def cpu_baseline(wl, sched, eps, sample):
+def cpu_baseline(wl, sched, eps, sample, pool=None):
     """The fp64 oracle (as it stands) on the first `sample` inputs."""
     from oracle.search import decode_workload
     try:
@@ -59,10 +60,10 @@ def cpu_baseline(wl, sched, eps, sample):
     cores = threads or len(os.sched_getaffinity(0))
     idx = np.arange(min(sample, len(wl.Lx)))
     t0 = time.perf_counter()
-    r = decode_workload(wl, sched=sched, eps=eps, inputs=idx)
+    r = decode_workload(wl, sched=sched, eps=eps, inputs=idx, pool=pool)
     dt = time.perf_counter() - t0
     return {"value": r.n_hyps / dt, "unit": "hyps/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {len(idx)} of {len(wl.Lx)} inputs, same n/k/eps/delta/M, numpy fp64 "
+            "sample": f"first {len(idx)} of {len(wl.Lx)} inputs, same n/k/eps/delta/M/pool, numpy fp64 "
                       f"({dt:.1f} s, {r.expansions} expansions)",
             "expansions_per_s": r.expansions / dt, "seconds": dt}
 
@@ -110,8 +111,10 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--sched", default="var_stream",
                     choices=["fixed", "fixed_stream", "fixed_fairseq", "fixed_fairseq_stream", "var_batch",
-                             "var_stream", "var_fifo"])
+                             "var_stream", "var_fifo", "var_cap"])
     ap.add_argument("--eps", type=float, default=None)
+    ap.add_argument("--pool", type=int, default=None,
+                    help="beams cached by var_cap (default 2n); rows per step stay <= n*k")
     ap.add_argument("--cpu-sample", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph-replay", action="store_true",
@@ -134,12 +137,15 @@ def main():
 
     cfg = get_config(args.config)
     eps = cfg.eps if args.eps is None else args.eps
-    if args.sched not in ("var_stream", "var_fifo", "fixed_stream", "fixed_fairseq_stream"):
+    if args.sched not in ("var_stream", "var_fifo", "fixed_stream", "fixed_fairseq_stream", "var_cap"):
         eps = 0.0
+    if args.pool is not None and args.sched != "var_cap":
+        ap.error("--pool applies to --sched var_cap only")
+    pool = (2 * cfg.n if args.pool is None else args.pool) if args.sched == "var_cap" else None
     wl = make_workload(cfg)
     weights = weights_to_device(wl)
     h0 = inputs_to_device(wl)
-    dec = decoder_for_workload(wl, sched=args.sched, eps=eps, weights=weights)
+    dec = decoder_for_workload(wl, sched=args.sched, eps=eps, weights=weights, pool=pool)
     N = len(wl.Lx)
 
     def run_once():
@@ -183,13 +189,13 @@ def main():
     proj_flops = 2.0 * cfg.d * cfg.V * st["expansions"] * args.steps
     achieved = proj_flops / (proj_ms * 1e-3) / 1e12 if proj_ms > 0 else 0.0
     peak = PEAK_TFLOPS[cfg.dtype]
-    workload_key = f"cfg{args.config} {args.sched} eps={eps:g}"
+    workload_key = f"cfg{args.config} {args.sched} eps={eps:g}" + (f" pool={pool}" if pool else "")
     out = {
         "metric": METRIC, "value": hyps_per_s, "unit": "hyps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": per_run * 1e3,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": _workload_desc(cfg, args.sched, eps), "key": workload_key, "inputs": N,
+        "config": {"workload": _workload_desc(cfg, args.sched, eps, pool), "key": workload_key, "inputs": N,
                    "parallelism": "single GPU"},
         "expansions_per_s": exps_per_s,
         "search": {k: st[k] for k in ("timesteps", "expansions", "noops", "refills", "hyps")},
@@ -206,7 +212,7 @@ def main():
     }
     dec.close()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.sched, eps, args.cpu_sample)
+        out["cpu_baseline"] = cpu_baseline(wl, args.sched, eps, args.cpu_sample, pool)
         out["gpu_over_cpu"] = hyps_per_s / out["cpu_baseline"]["value"]
     print(json.dumps(out), flush=True)
 

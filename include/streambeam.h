@@ -55,9 +55,17 @@ typedef enum {
  * timestep (the batch capacity n taken from the beam with the most steps
  * down; at most n beams are live). All four return the same outputs for
  * the same parameters (eps, delta, M as forced below). */
-typedef enum { SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2, SB_VAR_FIFO = 3, SB_FIXED_STREAM = 4 } sb_sched;
+typedef enum {
+  SB_FIXED = 0, SB_VAR_BATCH = 1, SB_VAR_STREAM = 2, SB_VAR_FIFO = 3, SB_FIXED_STREAM = 4, SB_VAR_CAP = 5
+} sb_sched;
 /* SB_FIXED_STREAM (App. A.1, Table 3): fixed-width search (delta=+inf, M=k)
- * with Var-Stream's refill and selection; its outputs equal SB_FIXED's. */
+ * with Var-Stream's refill and selection; its outputs equal SB_FIXED's.
+ * SB_VAR_CAP (Sec. 3, last paragraph; Sec. 4.2, 4.3): capacity-constrained
+ * Var-Stream. Up to params.pool >= n beams are cached; the refill test and
+ * amount use the pool size (refill when live <= eps*pool, up to pool beams);
+ * each timestep takes the live beams in order of (steps taken, admission)
+ * while their active candidates total at most n*k rows, stopping at the
+ * first beam that would exceed that limit. Outputs equal Var-Batch's. */
 
 /* Finalization rule (App. A.1, implementation differences to Fairseq).
  * SB_RULE_PAPER: terminated candidates stay on the beam through no-op
@@ -92,6 +100,10 @@ typedef struct {
   int32_t max_len_cap;   /* upper bound on every input's max_len, 1..4096         */
   int32_t max_inputs;    /* queue capacity (inputs per decoder lifetime/reset)    */
   int32_t finalize_rule; /* sb_rule; SB_RULE_FAIRSEQ forces delta=+inf, M=k       */
+  int32_t pool;          /* beams cached at once: 0 means n; with SB_VAR_CAP any
+                            value in [n, 4096], else it must be 0 or n. Beam and
+                            candidate storage scale with it, row buffers with
+                            n*k                                                   */
 } sb_params;
 
 /* Synthetic decoder D (Sec. 2). Token 0 is EOS and also the start symbol.

@@ -17,11 +17,11 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "streambeam.h")
 
 SB_OK, SB_E_INVALID_ARG, SB_E_WORKSPACE, SB_E_STATE, SB_E_QUEUE_FULL, SB_E_TRUNCATED, \
     SB_E_HIP, SB_E_UNSUPPORTED = range(8)
-SB_FIXED, SB_VAR_BATCH, SB_VAR_STREAM, SB_VAR_FIFO, SB_FIXED_STREAM = 0, 1, 2, 3, 4
+SB_FIXED, SB_VAR_BATCH, SB_VAR_STREAM, SB_VAR_FIFO, SB_FIXED_STREAM, SB_VAR_CAP = 0, 1, 2, 3, 4, 5
 SB_RULE_PAPER, SB_RULE_FAIRSEQ = 0, 1
 SB_F32, SB_BF16 = 0, 1
 SCHEDULERS = {"fixed": SB_FIXED, "var_batch": SB_VAR_BATCH, "var_stream": SB_VAR_STREAM,
-              "var_fifo": SB_VAR_FIFO, "fixed_stream": SB_FIXED_STREAM}
+              "var_fifo": SB_VAR_FIFO, "fixed_stream": SB_FIXED_STREAM, "var_cap": SB_VAR_CAP}
 # Scheduler names that also pick the Fairseq finalization rule.
 FAIRSEQ_SCHEDULERS = {"fixed_fairseq": SB_FIXED, "fixed_fairseq_stream": SB_FIXED_STREAM}
 
@@ -29,7 +29,7 @@ FAIRSEQ_SCHEDULERS = {"fixed_fairseq": SB_FIXED, "fixed_fairseq_stream": SB_FIXE
 class SbParams(ctypes.Structure):
     _fields_ = [("k", c_int32), ("n", c_int32), ("eps", c_double), ("delta", c_double),
                 ("max_per_node", c_int32), ("sched", c_int32), ("max_len_cap", c_int32),
-                ("max_inputs", c_int32), ("finalize_rule", c_int32)]
+                ("max_inputs", c_int32), ("finalize_rule", c_int32), ("pool", c_int32)]
 
 
 class SbModel(ctypes.Structure):

@@ -46,7 +46,7 @@ namespace {
 constexpr size_t ALIGN = 256;
 
 struct Layout {
-  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, s_status, s_score, s_tok, s_h,
+  size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
       o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, wout_t, total;
 };
@@ -55,10 +55,15 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int kbucket_of(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
 
+// Beam records held by the decoder: the cached pool (0 means n).
+int pool_of(const sb_params &p) { return p.pool > 0 ? p.pool : p.n; }
+
 Layout layout_of(const sb_model &m, const sb_params &p) {
   Layout L{};
   const size_t es = m.dtype == SB_BF16 ? 2 : 4;
-  const size_t n = p.n, k = p.k, d = m.d, nk = n * k, Rm = nk;
+  // Beams and candidate slots are sized by the pool of cached beams; the
+  // per-row buffers by the n*k rows a timestep may expand.
+  const size_t n = pool_of(p), k = p.k, d = m.d, nk = n * k, Rm = (size_t)p.n * k;
   const size_t S = proj_tiles(m.vocab);
   const size_t KB = kbucket_of(p.k + (p.finalize_rule == SB_RULE_FAIRSEQ ? 1 : 0));
   const size_t bpw = p.finalize_rule == SB_RULE_FAIRSEQ ? 2 * (size_t)p.k : (size_t)p.k;
@@ -79,6 +84,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.b_par = take(n * 4);
   L.b_ml = take(n * 4);
   L.b_nout = take(n * 4);
+  L.b_order = take(n * 4);
   L.s_status = take(nk * 4);
   L.s_score = take(nk * 8);
   L.s_tok = take(nk * 4);
@@ -127,7 +133,11 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   if (!(p->eps >= 0.0 && p->eps < 1.0)) return bad(SB_E_INVALID_ARG, "eps must be in [0, 1)");
   if (!(p->delta > 0.0)) return bad(SB_E_INVALID_ARG, "delta must be > 0 (use +inf to disable)");
   if (p->max_per_node < 1 || p->max_per_node > p->k) return bad(SB_E_INVALID_ARG, "max_per_node must be in [1, k]");
-  if (p->sched < SB_FIXED || p->sched > SB_FIXED_STREAM) return bad(SB_E_INVALID_ARG, "unknown scheduler");
+  if (p->sched < SB_FIXED || p->sched > SB_VAR_CAP) return bad(SB_E_INVALID_ARG, "unknown scheduler");
+  if (p->pool != 0 && p->pool != p->n && p->sched != SB_VAR_CAP)
+    return bad(SB_E_INVALID_ARG, "a pool other than n needs SB_VAR_CAP");
+  if (p->pool != 0 && (p->pool < p->n || p->pool > 4096)) return bad(SB_E_INVALID_ARG, "pool must be 0 or in [n, 4096]");
+  if ((int64_t)pool_of(*p) * p->k > 65536) return bad(SB_E_UNSUPPORTED, "pool*k must be <= 65536");
   if (p->finalize_rule != SB_RULE_PAPER && p->finalize_rule != SB_RULE_FAIRSEQ)
     return bad(SB_E_INVALID_ARG, "unknown finalization rule");
   if (p->finalize_rule == SB_RULE_FAIRSEQ && p->k > KMAX_SUPPORTED - 1)
@@ -135,8 +145,9 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   if (p->max_len_cap < 1 || p->max_len_cap > 4096) return bad(SB_E_INVALID_ARG, "max_len_cap must be in [1, 4096]");
   if (p->max_inputs < 1) return bad(SB_E_INVALID_ARG, "max_inputs must be >= 1");
   const int64_t es = m->dtype == SB_BF16 ? 2 : 4;
-  if ((int64_t)(m->vocab + 127) / 128 * 128 * m->d * es >= (1ll << 32) || (int64_t)p->n * p->k * m->d * es >= (1ll << 32))
-    return bad(SB_E_UNSUPPORTED, "W_out and the row-state buffer must each be under 4 GiB");
+  if ((int64_t)(m->vocab + 127) / 128 * 128 * m->d * es >= (1ll << 32) ||
+      (int64_t)pool_of(*p) * p->k * m->d * es >= (1ll << 32))
+    return bad(SB_E_UNSUPPORTED, "W_out and the candidate-state buffer must each be under 4 GiB");
   if (m->kv_layers < 0 || m->kv_layers > 8) return bad(SB_E_UNSUPPORTED, "kv_layers must be in [0, 8]");
   if (m->kv_layers > 0 && m->dtype != SB_BF16) return bad(SB_E_UNSUPPORTED, "KV state requires bf16");
   if (m->kv_layers > 0 && !m->W_kv) return bad(SB_E_INVALID_ARG, "W_kv is NULL");
@@ -296,6 +307,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.b_par = reinterpret_cast<int32_t *>(w + L.b_par);
   st.b_ml = reinterpret_cast<int32_t *>(w + L.b_ml);
   st.b_nout = reinterpret_cast<int32_t *>(w + L.b_nout);
+  st.b_order = reinterpret_cast<int32_t *>(w + L.b_order);
   st.s_status = reinterpret_cast<int32_t *>(w + L.s_status);
   st.s_score = reinterpret_cast<double *>(w + L.s_score);
   st.s_tok = reinterpret_cast<int32_t *>(w + L.s_tok);
@@ -327,13 +339,13 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.W_out = model->W_out;
   st.wout_t = w + L.wout_t;
   const sb_params &p = dec->params;
-  st.n = p.n;
+  st.n = pool_of(p);
   st.k = p.k;
   st.d = model->d;
   st.V = model->vocab;
   st.M = p.max_per_node;
   st.max_len_cap = p.max_len_cap;
-  st.refill_thr = (int32_t)floor(p.eps * (double)p.n);   // live <= eps*n  <=>  live <= floor(eps*n)
+  st.refill_thr = (int32_t)floor(p.eps * (double)st.n);   // live <= eps*P  <=>  live <= floor(eps*P)
   st.S = proj_tiles(model->vocab);
   st.R_max = p.n * p.k;
   st.dtype = model->dtype;
@@ -344,6 +356,8 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.kbucket = kbucket_of(p.k + st.rule);   // the Fairseq rule draws k+1 children per parent
   st.hist_width = std::max(16, (st.R_max + 63) / 64);
   st.select_all = p.sched == SB_VAR_FIFO ? 1 : 0;
+  st.cap = p.sched == SB_VAR_CAP ? 1 : 0;
+  st.row_budget = p.n * p.k;
   {
     int dev = 0, ncu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -440,7 +454,7 @@ sb_status sb_run(sb_decoder *dec) {
   if (!dec) return SB_E_INVALID_ARG;
   // Every step either expands a live beam or is the final no-op, and a beam
   // takes at most max_len_cap steps, so this bounds any correct run.
-  const int64_t limit = ((int64_t)dec->n_queued + dec->params.n) * (dec->params.max_len_cap + 1) + 64;
+  const int64_t limit = ((int64_t)dec->n_queued + pool_of(dec->params)) * (dec->params.max_len_cap + 1) + 64;
   const bool timed = dec->timing;
   if (!timed && !dec->graph_exec) {
     sb_status s = capture(dec, &dec->graph, &dec->graph_exec);

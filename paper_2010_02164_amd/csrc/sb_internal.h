@@ -44,13 +44,14 @@ struct DevState {
   // input queue
   void *q_h0;          // [max_inputs][d]
   int32_t *q_Lx, *q_ml;
-  // beams [n]
+  // beams [n] (n = the pool of cached beams)
   int32_t *b_input;    // queue position, -1 = free
   int32_t *b_steps;    // l_t: steps taken
   int32_t *b_sel;      // 1 if expanded this step
   int32_t *b_par;      // which KV buffer holds this beam's state
   int32_t *b_ml;       // max_len of the beam's input
   int32_t *b_nout;     // outputs already finalized (Fairseq rule)
+  int32_t *b_order;    // capacity mode: records of the live beams in admission order
   // candidate slots [n*k], slot = beam*k + rank
   int32_t *s_status;
   double *s_score;
@@ -90,6 +91,8 @@ struct DevState {
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   int32_t n_cu;        // compute units of the device (persistent launches)
   int32_t select_all;  // 1: expand every live beam (Var-Str-FIFO), 0: minimal l_t only
+  int32_t cap;         // 1: capacity-constrained selection (row_budget rows, (l_t, admission) order)
+  int32_t row_budget;  // rows a timestep may expand (batch size times k)
   int32_t rule;        // finalization rule: 0 paper (App. A.1), 1 Fairseq
   int32_t bpw;         // backpointer entries per level: k (paper), 2k (Fairseq: beam + outputs)
   double delta;

@@ -1,8 +1,10 @@
-// Scheduler kernel: refill/admission, beam selection by minimal l_t and
-// compaction of the active candidates of the selected beams into a dense
-// row list (Alg. 1: the refill branch, "select E_s, B_s with min l_t", and
-// the candidate loop's iteration space). One workgroup; the step's
-// decisions are taken on the device so no host round trip is needed.
+// Scheduler kernel: refill/admission, beam selection by minimal l_t (or
+// every live beam, or the capacity-constrained prefix) and compaction of the
+// active candidates of the selected beams into a dense row list (Alg. 1: the
+// refill branch, "select E_s, B_s with min l_t", and the candidate loop's
+// iteration space; Sec. 3's selection up to a limit on total beam width).
+// One workgroup; the step's decisions are taken on the device so no host
+// round trip is needed.
 #include "sb_internal.h"
 
 namespace sb {
@@ -59,6 +61,8 @@ __device__ int block_min(int v, int *sm) {
 // come out in beam order) and keeps their records in registers; every
 // decision needs one block-wide scan or reduction.
 constexpr int SCHED_MAXB = 4;
+constexpr int SCHED_MAXP = SCHED_THREADS * SCHED_MAXB;   // beam records
+constexpr int SCHED_MAXL = 4096;                         // l_t bins (max_len_cap)
 
 __device__ long long block_excl_scan64(long long v, long long *sm, long long *total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
@@ -86,15 +90,141 @@ __device__ long long block_excl_scan64(long long v, long long *sm, long long *to
   return res;
 }
 
+// Capacity-constrained selection works on the live beams in admission
+// order: b_order lists their records (the previous step's live beams, then
+// the ones admitted by that step). Its LDS scratch: per record (l_t << 8 |
+// active width), the new order list, the active width per l_t, the
+// selection flags, and the cut (l*, rows left at l*).
+struct CapSmem {
+  int info[SCHED_MAXP];
+  int ord[SCHED_MAXP];
+  int hist[SCHED_MAXL];
+  unsigned char sel[SCHED_MAXP];
+  int cut[2];
+};
+
+// Capacity-constrained selection (Sec. 3, last paragraph): the live beams
+// in order of (l_t, admission) are taken while their active candidates total
+// at most row_budget rows. Called by the whole workgroup after admission
+// with the thread's records (inp, stp) and its kept positions of the old
+// order list (orec); nlive = live beams after admission. Leaves cs.sel[b]
+// set for the selected records and writes the new order list to b_order.
+__device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *inp, const int *stp,
+                           const int *orec, int b0, int nb, int nlive) {
+  const int k = st.k;
+  // Kept positions are compacted in order ahead of the admitted beams.
+  int kept_l = 0;
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) kept_l += u < nb && orec[u] >= 0;
+  int kept_tot;
+  int pos = block_excl_scan(kept_l, sm, &kept_tot);
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u)
+    if (u < nb && orec[u] >= 0) cs.ord[pos++] = orec[u];
+  // Per record: l_t and active width (a fresh beam has one candidate).
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) {
+    if (u < nb) {
+      const int b = b0 + u;
+      cs.sel[b] = 0;
+      if (inp[u] >= 0) {
+        int w = 1;
+        if (stp[u] > 0) {
+          w = 0;
+          for (int j = 0; j < k; ++j) w += st.s_status[b * k + j] == SLOT_ACTIVE;
+        }
+        cs.info[b] = (stp[u] << 8) | w;
+      }
+    }
+  }
+  __syncthreads();
+  // New order list to memory; active width per l_t.
+  int oinfo[SCHED_MAXB], orid[SCHED_MAXB];
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) {
+    orid[u] = -1;
+    oinfo[u] = 0;
+    if (u < nb && b0 + u < nlive) {
+      orid[u] = cs.ord[b0 + u];
+      oinfo[u] = cs.info[orid[u]];
+      st.b_order[b0 + u] = orid[u];
+      atomicAdd(&cs.hist[min(oinfo[u] >> 8, st.max_len_cap - 1)], oinfo[u] & 0xff);   // live l_t < max_len
+    }
+  }
+  __syncthreads();
+  // The cut: l* = the first l_t whose cumulative width exceeds the budget;
+  // every beam below l* fits, none above it is taken.
+  const int L = st.max_len_cap, budget = st.row_budget;
+  const int bins = (L + SCHED_THREADS - 1) / SCHED_THREADS;
+  const int j0 = min(L, (int)threadIdx.x * bins), j1 = min(L, j0 + bins);
+  int hsum = 0;
+  for (int j = j0; j < j1; ++j) hsum += cs.hist[j];
+  int htot;
+  int cum = block_excl_scan(hsum, sm, &htot);
+  for (int j = j0; j < j1; ++j) {
+    const int h = cs.hist[j];
+    if (cum <= budget && cum + h > budget) {
+      cs.cut[0] = j;
+      cs.cut[1] = budget - cum;
+    }
+    cum += h;
+  }
+  __syncthreads();
+  const int lstar = cs.cut[0], rem = cs.cut[1];
+  // At l*, beams are taken in admission order while they fit.
+  int lv = 0;
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u)
+    if (orid[u] >= 0 && (oinfo[u] >> 8) == lstar) lv += oinfo[u] & 0xff;
+  int ltot;
+  int e = block_excl_scan(lv, sm, &ltot);
+#pragma unroll
+  for (int u = 0; u < SCHED_MAXB; ++u) {
+    if (orid[u] >= 0) {
+      const int s = oinfo[u] >> 8, w = oinfo[u] & 0xff;
+      bool take = s < lstar;
+      if (s == lstar) {
+        take = e + w <= rem;
+        e += w;
+      }
+      cs.sel[orid[u]] = take;
+    }
+  }
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
   __shared__ long long sm64[SCHED_THREADS / 64 + 1];
   __shared__ int sm[SCHED_THREADS / 64 + 1];
+  __shared__ CapSmem cs;
   DevCtrl *c = st.ctrl;
   const int tid = threadIdx.x;
   const int n = st.n, k = st.k;
   const int nq = c->n_queued, cursor = c->cursor;
   const int per = (n + SCHED_THREADS - 1) / SCHED_THREADS;   // <= SCHED_MAXB
   const int b0 = min(n, tid * per), nb = min(n, b0 + per) - b0;
+  const bool cap = st.cap != 0;
+
+  // Capacity mode: this thread's positions b0 .. b0+nb-1 of the order list
+  // (which holds the live + admitted count of the previous step), read
+  // before any record changes below; a beam that finished since is dropped.
+  int orec[SCHED_MAXB];
+  if (cap) {
+    const int nord = c->live;
+#pragma unroll
+    for (int u = 0; u < SCHED_MAXB; ++u) {
+      orec[u] = -1;
+      if (u < nb && b0 + u < nord) {
+        const int r = st.b_order[b0 + u];
+        if (st.b_input[r] >= 0) orec[u] = r;
+      }
+    }
+    for (int j = tid; j < st.max_len_cap; j += SCHED_THREADS) cs.hist[j] = 0;
+    if (tid == 0) {
+      cs.cut[0] = INT_MAX;
+      cs.cut[1] = 0;
+    }
+  }
 
   int inp[SCHED_MAXB], stp[SCHED_MAXB];
   int live_l = 0;
@@ -132,6 +262,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
           st.b_par[b] = 0;
           st.b_ml[b] = st.q_ml[inp[u]];
           st.b_nout[b] = 0;
+          if (cap) cs.ord[live + rank] = b;   // admitted beams follow the live ones
           for (int j = 0; j < k; ++j) {
             st.s_status[b * k + j] = j == 0 ? SLOT_ACTIVE : SLOT_EMPTY;
             st.s_score[b * k + j] = 0.0;
@@ -145,12 +276,13 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
 
   // Selection: the live beams with the fewest steps taken, or every live
   // beam (Var-Str-FIFO: the capacity n, from the beam with the most steps
-  // down, covers all of them).
+  // down, covers all of them), or the capacity-constrained prefix.
   int mn_l = INT_MAX;
 #pragma unroll
   for (int u = 0; u < SCHED_MAXB; ++u)
     if (u < nb && inp[u] >= 0) mn_l = min(mn_l, stp[u]);
   const int mn = block_min(mn_l, sm);
+  if (cap) cap_select(st, cs, sm, inp, stp, orec, b0, nb, live + admit);
 
   // Active and terminated candidates of the selected beams (slot order);
   // each beam's active slots are kept as a bit mask.
@@ -159,7 +291,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
 #pragma unroll
   for (int u = 0; u < SCHED_MAXB; ++u) {
     amask[u] = 0u;
-    const bool sel = u < nb && inp[u] >= 0 && (st.select_all || stp[u] == mn);
+    const bool sel = u < nb && inp[u] >= 0 && (cap ? cs.sel[b0 + u] != 0 : (st.select_all || stp[u] == mn));
     sel_l += sel;
     if (sel) {
       for (int j = 0; j < k; ++j) {
@@ -179,7 +311,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
   for (int u = 0; u < SCHED_MAXB; ++u) {
     if (u < nb) {
       const int b = b0 + u;
-      const bool sel = inp[u] >= 0 && (st.select_all || stp[u] == mn);
+      const bool sel = inp[u] >= 0 && (cap ? cs.sel[b] != 0 : (st.select_all || stp[u] == mn));
       st.b_sel[b] = sel;
       const int lx = sel ? st.q_Lx[inp[u]] : 0;
       for (int j = 0; j < k; ++j) {

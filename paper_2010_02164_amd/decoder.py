@@ -39,9 +39,11 @@ def _check(status: int, where: str, dec_handle=None):
     raise N.StreambeamError(status, where, detail)
 
 
-def make_params(k, n, eps, delta, M, sched, max_len_cap, max_inputs, rule=None) -> N.SbParams:
+def make_params(k, n, eps, delta, M, sched, max_len_cap, max_inputs, rule=None, pool=None) -> N.SbParams:
     """sched: a scheduler name (N.SCHEDULERS, or N.FAIRSEQ_SCHEDULERS, which
-    also select the Fairseq finalization rule) or an sb_sched value."""
+    also select the Fairseq finalization rule) or an sb_sched value. pool:
+    beams cached by the capacity-constrained scheduler ("var_cap"; None
+    means n)."""
     if isinstance(sched, str) and sched in N.FAIRSEQ_SCHEDULERS:
         code, rule = N.FAIRSEQ_SCHEDULERS[sched], N.SB_RULE_FAIRSEQ
     else:
@@ -49,7 +51,8 @@ def make_params(k, n, eps, delta, M, sched, max_len_cap, max_inputs, rule=None) 
     return N.SbParams(k=int(k), n=int(n), eps=float(eps),
                       delta=float(math.inf if delta is None else delta), max_per_node=int(M),
                       sched=code, max_len_cap=int(max_len_cap), max_inputs=int(max_inputs),
-                      finalize_rule=int(N.SB_RULE_PAPER if rule is None else rule))
+                      finalize_rule=int(N.SB_RULE_PAPER if rule is None else rule),
+                      pool=0 if pool is None else int(pool))
 
 
 def make_model(vocab, d, dtype, beta, W_h=0, E=0, W_out=0, kv_layers=0, W_kv=0) -> N.SbModel:
@@ -71,7 +74,8 @@ class Decoder:
 
     def __init__(self, W_h, E, W_out, *, beta: float, k: int, n: int, eps: float = 0.0,
                  delta: Optional[float] = None, M: Optional[int] = None, sched: str = "var_stream",
-                 max_len_cap: int = 256, max_inputs: int = 1024, W_kv=None, stream=None):
+                 max_len_cap: int = 256, max_inputs: int = 1024, W_kv=None, stream=None,
+                 pool: Optional[int] = None):
         import torch
         self.torch = torch
         if not torch.cuda.is_available():
@@ -88,7 +92,8 @@ class Decoder:
         self.model = make_model(V, d, self.dtype, beta, W_h.data_ptr(), E.data_ptr(), W_out.data_ptr(),
                                 0 if W_kv is None else W_kv.shape[0],
                                 0 if W_kv is None else W_kv.data_ptr())
-        self.params = make_params(k, n, eps, delta, k if M is None else M, sched, max_len_cap, max_inputs)
+        self.params = make_params(k, n, eps, delta, k if M is None else M, sched, max_len_cap, max_inputs,
+                                  pool=pool)
         L = N.lib()
         _check(L.sb_validate(ctypes.byref(self.model), ctypes.byref(self.params)), "sb_validate")
         nbytes = workspace_bytes(self.model, self.params)
@@ -252,7 +257,11 @@ def inputs_to_device(wl, idx=None, device="cuda"):
 
 def decoder_for_workload(wl, sched="var_stream", eps=None, n=None, max_inputs=None, weights=None,
                          **kw) -> Decoder:
+    """A decoder for a synthgen workload with its config's parameters; the
+    capacity-constrained scheduler caches 2n beams unless `pool` is given."""
     c = wl.cfg
+    if sched == "var_cap" and kw.get("pool") is None:
+        kw["pool"] = 2 * (c.n if n is None else n)
     W_h, E, W_out, W_kv = weights if weights is not None else weights_to_device(wl)
     return Decoder(W_h, E, W_out, W_kv=W_kv, beta=c.beta, k=c.k, n=c.n if n is None else n,
                    eps=c.eps if eps is None else eps, delta=c.delta, M=c.M, sched=sched,

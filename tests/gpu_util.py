@@ -8,13 +8,14 @@ from oracle.compare import compare
 from oracle.search import decode_workload
 
 
-def gpu_decode(wl, sched, eps=None, n=None, inputs=None, weights=None, timing=False):
+def gpu_decode(wl, sched, eps=None, n=None, inputs=None, weights=None, timing=False, pool=None):
     """Run the HIP decoder over (a subset of) a workload; returns
     (per-input hypotheses, stats, decoder)."""
     import torch
     from paper_2010_02164_amd import decoder_for_workload, group_by_input, inputs_to_device
     idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
-    dec = decoder_for_workload(wl, sched=sched, eps=eps, n=n, max_inputs=len(idx), weights=weights)
+    dec = decoder_for_workload(wl, sched=sched, eps=eps, n=n, max_inputs=len(idx), weights=weights,
+                               pool=pool)
     if timing:
         dec.set_timing(True)
     dec.submit(inputs_to_device(wl, idx), wl.Lx[idx], wl.max_len[idx])
@@ -30,15 +31,15 @@ def score_tol(wl):
 
 
 def check_parity(wl, sched, eps=None, n=None, inputs=None, oracle_res=None, weights=None,
-                 require_stats=True):
+                 require_stats=True, pool=None):
     """GPU vs oracle on the same inputs; returns the comparison report."""
     idx = np.arange(len(wl.Lx)) if inputs is None else np.asarray(inputs)
-    o = oracle_res or decode_workload(wl, sched=sched, eps=eps, n=n, inputs=idx)
-    g, st, dec = gpu_decode(wl, sched, eps=eps, n=n, inputs=idx, weights=weights)
+    o = oracle_res or decode_workload(wl, sched=sched, eps=eps, n=n, inputs=idx, pool=pool)
+    g, st, dec = gpu_decode(wl, sched, eps=eps, n=n, inputs=idx, weights=weights, pool=pool)
     dec.close()
     rep = compare(o.hyps, o.min_margin, [[(h.tokens, h.score, h.status) for h in y] for y in g],
                   inputs=idx, score_tol=score_tol(wl))
-    print(f"[parity] {wl.cfg.name} {sched} eps={eps} n={n} N={len(idx)}: {rep.summary()}", flush=True)
+    print(f"[parity] {wl.cfg.name} {sched} eps={eps} n={n} pool={pool} N={len(idx)}: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures[:5]
     if require_stats and rep.n_excused == 0:
         for key in ("timesteps", "expansions", "noops", "refills", "admitted"):

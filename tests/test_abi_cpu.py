@@ -46,6 +46,8 @@ def test_workspace_sizes(native_lib, i):
     (dict(max_inputs=0), N.SB_E_INVALID_ARG), (dict(vocab=3), N.SB_E_INVALID_ARG),
     (dict(n=0), N.SB_E_UNSUPPORTED), (dict(kv_layers=2), N.SB_E_UNSUPPORTED),
     (dict(finalize_rule=2), N.SB_E_INVALID_ARG), (dict(k=16, finalize_rule=1), N.SB_E_UNSUPPORTED),
+    (dict(pool=256), N.SB_E_INVALID_ARG), (dict(sched=5, pool=64), N.SB_E_INVALID_ARG),
+    (dict(sched=5, pool=4097), N.SB_E_INVALID_ARG), (dict(sched=6), N.SB_E_INVALID_ARG),
 ])
 def test_validate_rejects(native_lib, over, code):
     m, p = _mp(CONFIGS[3], **over)
@@ -60,6 +62,21 @@ def test_fairseq_rule_workspace(native_lib):
     c = CONFIGS[3]
     assert native_lib.sb_validate(ctypes.byref(m2), ctypes.byref(p2)) == N.SB_OK
     assert workspace_bytes(m2, p2) >= workspace_bytes(m, p) + c.N * c.max_len_cap * c.k * 4
+
+
+def test_capacity_pool_workspace(native_lib):
+    # Beam and candidate storage scale with the pool of cached beams; the row
+    # buffers stay at n*k rows.
+    c = CONFIGS[3]
+    m, p = _mp(c)
+    m2, p2 = _mp(c, sched=N.SB_VAR_CAP, pool=2 * c.n)
+    m3, p3 = _mp(c, sched=N.SB_VAR_CAP, pool=0)
+    assert native_lib.sb_validate(ctypes.byref(m2), ctypes.byref(p2)) == N.SB_OK
+    assert native_lib.sb_validate(ctypes.byref(m3), ctypes.byref(p3)) == N.SB_OK
+    assert workspace_bytes(m3, p3) == workspace_bytes(m, p)
+    extra = workspace_bytes(m2, p2) - workspace_bytes(m, p)
+    slot_state = c.n * c.k * c.d * 4
+    assert slot_state <= extra < 2 * slot_state
 
 
 def test_delta_inf_is_valid(native_lib):

@@ -10,7 +10,7 @@ from tests.gpu_util import check_parity, gpu_decode
 pytestmark = pytest.mark.gpu
 
 SCHEDS = ["fixed", "var_batch", "var_stream", "var_fifo", "fixed_stream", "fixed_fairseq",
-          "fixed_fairseq_stream"]
+          "fixed_fairseq_stream", "var_cap"]
 
 
 @pytest.mark.parametrize("sched", SCHEDS)
@@ -25,7 +25,7 @@ def test_cfg2_reduced(gpu, sched):
     check_parity(wl, sched)
 
 
-@pytest.mark.parametrize("sched", ["var_batch", "var_stream", "var_fifo", "fixed_fairseq_stream"])
+@pytest.mark.parametrize("sched", ["var_batch", "var_stream", "var_fifo", "fixed_fairseq_stream", "var_cap"])
 def test_cfg3_reduced(gpu, sched):
     wl = make_workload(scaled(3, N=40, n=16, V=8000))
     check_parity(wl, sched)
@@ -56,13 +56,37 @@ def test_stream_equals_batch_bitwise_across_row_tilings(gpu):
     a, sa, da = gpu_decode(wl, "var_batch")
     b, sb, _ = gpu_decode(wl, "var_stream")
     f, sf, _ = gpu_decode(wl, "var_fifo", n=45)
+    p, sp, _ = gpu_decode(wl, "var_cap", n=50, pool=150)
     counts, width = da.rows_histogram()
     assert sum(c for i, c in enumerate(counts) if i * width > 256) > 0   # some steps use 256-row tiles
     for ya, yb, yf in zip(a, b, f):
         key = [(h.tokens, h.score, h.status) for h in ya]
         assert key == [(h.tokens, h.score, h.status) for h in yb]
         assert key == [(h.tokens, h.score, h.status) for h in yf]
-    assert sa["expansions"] == sb["expansions"] == sf["expansions"]
+    for ya, yp in zip(a, p):
+        assert [(h.tokens, h.score, h.status) for h in ya] == [(h.tokens, h.score, h.status) for h in yp]
+    assert sa["expansions"] == sb["expansions"] == sf["expansions"] == sp["expansions"]
+
+
+@pytest.mark.parametrize("n,pool,eps", [(3, 12, 0.25), (4, 9, 0.5), (2, 40, 0.0)])
+def test_capacity_limit_binding(gpu, n, pool, eps):
+    # Small n*k row limits against large pools: most timesteps stop at the
+    # limit, at a beam chosen by (l_t, admission order).
+    wl = make_workload(scaled(1, N=64))
+    check_parity(wl, "var_cap", eps=eps, n=n, pool=pool)
+
+
+def test_capacity_pool_of_n_is_fifo_on_gpu(gpu):
+    # With the pool equal to n every live beam fits the n*k limit: the
+    # capacity scheduler runs Var-Str-FIFO's schedule step for step.
+    wl = make_workload(scaled(2, N=200, n=64))
+    a, sa, da = gpu_decode(wl, "var_fifo", eps=0.25)
+    b, sb, db = gpu_decode(wl, "var_cap", eps=0.25, pool=64)
+    assert sa == sb
+    assert da.rows_histogram() == db.rows_histogram()
+    for ya, yb in zip(a, b):
+        assert [(h.tokens, h.score, h.status, h.finalize_step) for h in ya] == \
+               [(h.tokens, h.score, h.status, h.finalize_step) for h in yb]
 
 
 def test_fairseq_rule_stream_equals_batch_on_gpu_bitwise(gpu):
