@@ -13,6 +13,11 @@ The paper's decoder D(e_i, y_i) scores the next token of a partial output
 All arithmetic is float64. Weights arrive as float32 arrays whose values
 (bf16-exact for bf16 workloads) are held exactly in float64, so for bf16
 workloads the pre-activation W_h h + E[y] is an exact sum of exact products.
+
+AttnDecoder adds a length-dependent step (the decoder self-attention whose
+cost grows with the output position, App. A.2 and its Fig. 2): the
+candidate's state also holds its KV rows, and the projection reads
+x = bf16_rne(h + mean over layers of attention(h; K_l, V_l)).
 """
 from __future__ import annotations
 
@@ -98,3 +103,67 @@ class ElmanDecoder:
             raise ValueError("decoder has no KV state")
         out = np.einsum("i,ljio->ljo", np.asarray(h, np.float64), self.W_kv)
         return bf16_round(out)
+
+
+class AttnDecoder(ElmanDecoder):
+    """Elman decoder whose projection input adds a self-attention read-out
+    over the candidate's own KV rows (bf16 workloads with W_kv).
+
+    A candidate's state is (h, K, V) with K, V of shape [L, t, d]: the rows
+    bf16_rne(h_s . W_kv[l, 0]) and bf16_rne(h_s . W_kv[l, 1]) of the states
+    h_s of its first t tokens. One step, for a candidate emitting token t:
+        h     = bf16_rne(tanh(W_h h_prev + E[y]))          as ElmanDecoder
+        K, V  += the rows of h                             position t - 1
+        a_l   = sum_s softmax_s(K_l[s] . h / sqrt(d)) V_l[s]   s = 0 .. t-1
+        x     = bf16_rne(h + (1/L) sum_l a_l)
+        z     = W_out x ;  z[0] += beta (t - L_x)
+    The next step's recurrence reads h, not x.
+    """
+
+    def __init__(self, *a, **kw):
+        super().__init__(*a, **kw)
+        if self.W_kv is None or not self.bf16_state:
+            raise ValueError("attention needs bf16 states and W_kv")
+        self.L = self.W_kv.shape[0]
+
+    def initial_state(self, h0):
+        z = np.zeros((self.L, 0, self.d))
+        return (np.asarray(h0, dtype=np.float64), z, z)
+
+    def attention(self, h, K, V):
+        """(1/L) sum_l a_l for one candidate: h [d], K, V [L, t, d]."""
+        out = np.zeros(self.d)
+        for l in range(self.L):
+            s = K[l] @ h / np.sqrt(self.d)
+            w = np.exp(s - np.max(s))
+            out += (w / np.sum(w)) @ V[l]
+        return out / self.L
+
+    def expand(self, states, y, t, Lx, chunk: int = 256):
+        """One step for R candidates: returns (new states, lp [R,V])."""
+        R = len(states)
+        h = self.next_state(np.stack([st[0] for st in states]), np.asarray(y))
+        t, Lx = np.asarray(t), np.asarray(Lx)
+        x = np.empty((R, self.d))
+        new = []
+        for r, (_, K, V) in enumerate(states):
+            if K.shape[1] != t[r] - 1:
+                raise ValueError("KV rows do not match the output position")
+            kv = self.kv_row(h[r])                       # [L, 2, d]
+            K2 = np.concatenate([K, kv[:, 0:1]], axis=1)
+            V2 = np.concatenate([V, kv[:, 1:2]], axis=1)
+            x[r] = bf16_round(h[r] + self.attention(h[r], K2, V2))
+            new.append((h[r], K2, V2))
+        lp = np.empty((R, self.V))
+        for a in range(0, R, chunk):
+            b = min(R, a + chunk)
+            lp[a:b] = log_softmax(self.logits(x[a:b], t[a:b], Lx[a:b]))
+        return new, lp
+
+
+def decoder_for_workload(wl):
+    """The oracle decoder of a synthgen workload (AttnDecoder when the
+    config enables attention)."""
+    c = wl.cfg
+    cls = AttnDecoder if getattr(c, "attn", False) else ElmanDecoder
+    return cls(wl.W_h, wl.E, wl.W_out, c.beta, c.dtype == "bf16", wl.W_kv)

@@ -143,7 +143,7 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
         # selected beams (the inner loops of Alg. 1).
         rows = [(bi, j) for bi, b in enumerate(sel)
                 for j, cand in enumerate(b.cands) if cand.status == ACTIVE]
-        h_prev = np.stack([sel[bi].cands[j].h for bi, j in rows])
+        h_prev = [sel[bi].cands[j].h for bi, j in rows]
         y = np.array([sel[bi].cands[j].y for bi, j in rows])
         t = np.array([sel[bi].steps + 1 for bi, _ in rows])
         lx = np.array([Lx[sel[bi].input] for bi, _ in rows])
@@ -199,9 +199,9 @@ def decode_workload(wl, n=None, eps=None, k=None, delta=None, M=None, sched="var
     config's parameters; `sched` picks Fixed / Fixed-Stream / Fixed-Fairseq /
     Var-Batch / Var-Stream / Var-Str-FIFO ("var_fifo") / capacity-constrained
     Var-Stream ("var_cap", `pool` cached beams, default 2n)."""
-    from .decoder import ElmanDecoder
+    from .decoder import decoder_for_workload
     c = wl.cfg
-    dec = decoder or ElmanDecoder.from_workload(wl)
+    dec = decoder or decoder_for_workload(wl)
     n = c.n if n is None else n
     k = c.k if k is None else k
     eps = c.eps if eps is None else eps

@@ -1,4 +1,4 @@
-"""The five synthetic decoding workloads.
+"""The synthetic decoding workloads (five, plus config 5 with self-attention).
 
 Each config fixes the shape of a synthetic Elman decoder (state size d,
 vocabulary |V| with token 0 = EOS = start symbol), its storage dtype, the
@@ -34,6 +34,7 @@ class SearchConfig:
     len_hi: int            # uniform upper bound / lognormal clip upper bound
     max_len: Optional[int] # fixed max length, or None for floor(1.2 L_x + 10)
     kv_layers: int = 0     # per-candidate KV-like state (layers x {K,V} x t x d)
+    attn: bool = False     # the projection reads h plus the self-attention read-out over the KV rows
     seed: int = 0
     mu: float = 3.2        # lognormal location
     sigma: float = 0.5     # lognormal scale
@@ -81,6 +82,10 @@ CONFIGS = {
             lengths="lognormal", len_lo=3, len_hi=200, max_len=None,
             kv_layers=6),
 }
+# Length-dependent decoder step: config 5 (same weights and inputs) whose
+# projection input adds each layer's attention over the candidate's KV rows,
+# so a step's cost grows with the output position.
+CONFIGS[6] = CONFIGS[5].with_(name="kv_attn", attn=True)
 # Config 5 reuses config 4's per-input stream (same h0 / L_x / max_len).
 INPUT_SEED_OVERRIDE = {5: CONFIGS[4].seed}
 

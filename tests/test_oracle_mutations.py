@@ -14,6 +14,7 @@ import pytest
 
 import oracle.decoder
 import oracle.search
+import tests.test_oracle_attention as tattn
 import tests.test_oracle_decoder as tdec
 import tests.test_oracle_search as tsearch
 
@@ -51,6 +52,10 @@ PINS = {
     "cap_schedule": tsearch.test_capacity_schedule,
     "cap_replay": lambda: tsearch.test_capacity_schedule_event_replay(0.25, 12),
     "stream_vs_batch": lambda: tsearch.test_var_stream_matches_var_batch(0, 4, 0.25),
+    "attn_single": lambda: tattn.test_single_position_reads_its_value_row(0),
+    "attn_uniform": lambda: tattn.test_uniform_scores_average_the_value_rows(0),
+    "attn_two": lambda: tattn.test_two_positions_logistic_form(1),
+    "attn_recurrence": tattn.test_recurrence_reads_h_not_the_attention_input,
 }
 
 MUTATIONS = [
@@ -78,6 +83,16 @@ MUTATIONS = [
      "for score, j, w in pool[:2 * k]:", ["fairseq"]),
     ("fairseq_beam_keeps_terminated", "beam", "        if terminated(w):\n            continue\n", "",
      ["fairseq", "fairseq_exhaustive"]),
+    ("attn_scale_dropped", "decoder", "s = K[l] @ h / np.sqrt(self.d)", "s = K[l] @ h", ["attn_two"]),
+    ("attn_keys_as_values", "decoder", "out += (w / np.sum(w)) @ V[l]", "out += (w / np.sum(w)) @ K[l]",
+     ["attn_single", "attn_uniform"]),
+    ("attn_layers_summed", "decoder", "return out / self.L", "return out", ["attn_single", "attn_two"]),
+    ("attn_excludes_new_row", "decoder", "self.attention(h[r], K2, V2)", "self.attention(h[r], K, V)",
+     ["attn_single", "attn_two"]),
+    ("attn_state_carries_x", "decoder", "new.append((h[r], K2, V2))", "new.append((x[r], K2, V2))",
+     ["attn_recurrence"]),
+    ("attn_input_not_rounded", "decoder", "x[r] = bf16_round(h[r] + self.attention(h[r], K2, V2))",
+     "x[r] = h[r] + self.attention(h[r], K2, V2)", ["attn_single"]),
     ("refill_strict", "search", "len(live) <= eps * P", "len(live) < eps * P", ["fig1", "cap_schedule"]),
     ("refill_against_n", "search", "len(live) <= eps * P", "len(live) <= eps * n", ["cap_schedule"]),
     ("refill_to_n", "search", "m = min(P - len(live), N - c)", "m = min(n - len(live), N - c)",
@@ -100,8 +115,8 @@ MUTATIONS = [
 def test_planted_mistake_is_caught(monkeypatch, name, modname, old, new, pins):
     mut = _mutant(modname, old, new)
     if modname == "decoder":
-        for target in (oracle.decoder, tdec, tsearch):
-            for attr in ("ElmanDecoder", "log_softmax"):
+        for target in (oracle.decoder, tdec, tsearch, tattn):
+            for attr in ("ElmanDecoder", "AttnDecoder", "log_softmax", "decoder_for_workload"):
                 if hasattr(target, attr):
                     monkeypatch.setattr(target, attr, getattr(mut, attr))
     elif modname == "beam":
