@@ -112,7 +112,14 @@ typedef struct {
  *   E     [vocab][d] token embeddings
  *   W_out [vocab][d] z[v] = sum_j W_out[v][j] h[j]
  *   W_kv  [kv_layers][2][d][d] (bf16 only, or NULL): each expansion appends
- *         the rows bf16(h . W_kv[l][j]) to the candidate's KV-like state. */
+ *         the rows bf16(h . W_kv[l][j]) to the candidate's KV-like state.
+ * With attn = 1 (length-dependent step, App. A.2 and Fig. 2: decoder
+ * self-attention) the projection reads x instead of h:
+ *   a_l = sum_s softmax_s(K_l[s] . h / sqrt(d)) V_l[s] over the candidate's
+ *         KV rows s = 0 .. t-1, the row of this step included (K_l, V_l =
+ *         planes j = 0, 1 of layer l);
+ *   x   = bf16(h + (1/L) sum_l a_l), computed in fp64 and rounded once.
+ * The recurrence keeps reading h. */
 typedef struct {
   int32_t vocab;         /* |V| >= 2                                               */
   int32_t d;             /* state size in [64, 4096], a multiple of 64 (fp32) or
@@ -122,6 +129,8 @@ typedef struct {
   const void *W_h, *E, *W_out;
   int32_t kv_layers;     /* 0, or 1..8 with dtype SB_BF16                          */
   const void *W_kv;
+  int32_t attn;          /* 0, or 1: attention read-out (needs kv_layers > 0 and
+                            d in {256, 512, 1024, 2048})                          */
 } sb_model;
 
 /* One finalized hypothesis y_ij of Y[i] (Alg. 1 output). */
@@ -220,7 +229,8 @@ sb_status sb_timing(sb_decoder *dec, double *proj_ms, int64_t *proj_launches);
  * h_prev: device [R][d] (model dtype); y, t, L_x: host [R] (last token,
  * 1-based emitted position, input length); R <= n*k. Outputs: h_out device
  * [R][d] (model dtype), lse host [R], top_lp host [R][k] (log-probabilities
- * of the row's best k tokens, best first), top_tok host [R][k]. */
+ * of the row's best k tokens, best first), top_tok host [R][k].
+ * SB_E_UNSUPPORTED on a model with attn = 1 (its step needs KV history). */
 sb_status sb_debug_expand(sb_decoder *dec, int32_t R, const void *h_prev, const int32_t *y,
                           const int32_t *t, const int32_t *L_x, void *h_out, double *lse,
                           double *top_lp, int32_t *top_tok);

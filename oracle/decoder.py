@@ -109,9 +109,10 @@ class AttnDecoder(ElmanDecoder):
     """Elman decoder whose projection input adds a self-attention read-out
     over the candidate's own KV rows (bf16 workloads with W_kv).
 
-    A candidate's state is (h, K, V) with K, V of shape [L, t, d]: the rows
-    bf16_rne(h_s . W_kv[l, 0]) and bf16_rne(h_s . W_kv[l, 1]) of the states
-    h_s of its first t tokens. One step, for a candidate emitting token t:
+    A candidate's state is (h, chain): chain holds the KV rows [L, 2, d] of
+    the states h_s of its first t tokens, bf16_rne(h_s . W_kv[l, j]), as a
+    linked list shared with its ancestors (kv() stacks them into K, V of
+    shape [L, t, d]). One step, for a candidate emitting token t:
         h     = bf16_rne(tanh(W_h h_prev + E[y]))          as ElmanDecoder
         K, V  += the rows of h                             position t - 1
         a_l   = sum_s softmax_s(K_l[s] . h / sqrt(d)) V_l[s]   s = 0 .. t-1
@@ -127,8 +128,16 @@ class AttnDecoder(ElmanDecoder):
         self.L = self.W_kv.shape[0]
 
     def initial_state(self, h0):
-        z = np.zeros((self.L, 0, self.d))
-        return (np.asarray(h0, dtype=np.float64), z, z)
+        return (np.asarray(h0, dtype=np.float64), None)
+
+    def kv(self, state):
+        """(K, V), each [L, t, d], of a candidate state, positions in order."""
+        rows, chain = [], state[1]
+        while chain is not None:
+            chain, row = chain
+            rows.append(row)
+        a = np.stack(rows[::-1]) if rows else np.zeros((0, self.L, 2, self.d))
+        return a[:, :, 0].transpose(1, 0, 2), a[:, :, 1].transpose(1, 0, 2)
 
     def attention(self, h, K, V):
         """(1/L) sum_l a_l for one candidate: h [d], K, V [L, t, d]."""
@@ -146,14 +155,13 @@ class AttnDecoder(ElmanDecoder):
         t, Lx = np.asarray(t), np.asarray(Lx)
         x = np.empty((R, self.d))
         new = []
-        for r, (_, K, V) in enumerate(states):
-            if K.shape[1] != t[r] - 1:
+        for r, (_, chain) in enumerate(states):
+            st = (h[r], (chain, self.kv_row(h[r])))      # this step's rows appended
+            K, V = self.kv(st)
+            if K.shape[1] != t[r]:
                 raise ValueError("KV rows do not match the output position")
-            kv = self.kv_row(h[r])                       # [L, 2, d]
-            K2 = np.concatenate([K, kv[:, 0:1]], axis=1)
-            V2 = np.concatenate([V, kv[:, 1:2]], axis=1)
-            x[r] = bf16_round(h[r] + self.attention(h[r], K2, V2))
-            new.append((h[r], K2, V2))
+            x[r] = bf16_round(h[r] + self.attention(h[r], K, V))
+            new.append(st)
         lp = np.empty((R, self.V))
         for a in range(0, R, chunk):
             b = min(R, a + chunk)

@@ -35,7 +35,7 @@ class SbParams(ctypes.Structure):
 class SbModel(ctypes.Structure):
     _fields_ = [("vocab", c_int32), ("d", c_int32), ("dtype", c_int32), ("eos_beta", ctypes.c_float),
                 ("W_h", c_void_p), ("E", c_void_p), ("W_out", c_void_p),
-                ("kv_layers", c_int32), ("W_kv", c_void_p)]
+                ("kv_layers", c_int32), ("W_kv", c_void_p), ("attn", c_int32)]
 
 
 class SbHyp(ctypes.Structure):

@@ -48,7 +48,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, wout_t, total;
+      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, xbuf, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -113,6 +113,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
     L.kvnew = take(Rm * planes * d * 2);
     L.wkvT = take(planes * d * d * 2);
   }
+  if (m.attn) L.xbuf = take(Rm * d * 2);
   L.total = off;
   return L;
 }
@@ -151,6 +152,10 @@ sb_status check(const sb_model *m, const sb_params *p, std::string *why) {
   if (m->kv_layers < 0 || m->kv_layers > 8) return bad(SB_E_UNSUPPORTED, "kv_layers must be in [0, 8]");
   if (m->kv_layers > 0 && m->dtype != SB_BF16) return bad(SB_E_UNSUPPORTED, "KV state requires bf16");
   if (m->kv_layers > 0 && !m->W_kv) return bad(SB_E_INVALID_ARG, "W_kv is NULL");
+  if (m->attn != 0 && m->attn != 1) return bad(SB_E_INVALID_ARG, "attn must be 0 or 1");
+  if (m->attn && m->kv_layers == 0) return bad(SB_E_INVALID_ARG, "attention needs a KV state");
+  if (m->attn && m->d != 256 && m->d != 512 && m->d != 1024 && m->d != 2048)
+    return bad(SB_E_UNSUPPORTED, "attention needs d in {256, 512, 1024, 2048}");
   return SB_OK;
 }
 
@@ -199,6 +204,7 @@ sb_status launch_step(sb_decoder *dec, hipStream_t s, hipEvent_t e0 = nullptr, h
   HIPCHK(launch_sched(st, s));
   HIPCHK(launch_rec(st, s));
   if (st.kv_layers > 0) HIPCHK(launch_kv_append(st, s));
+  if (st.attn) HIPCHK(launch_attn(st, s));
   if (e0) HIPCHK(hipEventRecord(e0, s));
   HIPCHK(launch_proj(st, s));
   if (e1) HIPCHK(hipEventRecord(e1, s));
@@ -334,6 +340,9 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
     st.kvnew = reinterpret_cast<uint16_t *>(w + L.kvnew);
     st.wkvT = reinterpret_cast<uint16_t *>(w + L.wkvT);
   }
+  st.attn = model->attn;
+  st.xbuf = model->attn ? w + L.xbuf : nullptr;
+  st.proj_in = model->attn ? st.xbuf : st.hbuf;
   st.W_h = model->W_h;
   st.E = model->E;
   st.W_out = model->W_out;
@@ -611,6 +620,7 @@ sb_status sb_debug_expand(sb_decoder *dec, int32_t R, const void *h_prev, const 
   const DevState &st = dec->st;
   if (R < 1 || R > st.R_max || !h_prev || !y || !t || !L_x || !h_out || !lse || !top_lp || !top_tok)
     return SB_E_INVALID_ARG;
+  if (st.attn) return SB_E_UNSUPPORTED;
   const size_t es = st.dtype == 1 ? 2 : 4;
   const size_t rowbytes = (size_t)st.d * es;
   std::vector<int32_t> src(R);

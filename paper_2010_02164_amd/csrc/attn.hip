@@ -1,0 +1,184 @@
+// Length-dependent decoder step: the projection input of a row is
+// x = bf16(h + (1/L) sum_l a_l), a_l = sum_s softmax_s(K_l[s] . h / sqrt(d)) V_l[s]
+// over the candidate's own KV rows s = 0 .. t-1 (its history in the slot's
+// KV buffer, the current step's row in kvnew). This is the self-attention
+// whose cost grows with the output position (App. A.2, Fig. 2).
+//
+// All arithmetic after the bf16 loads is fp64: products of bf16 values are
+// exact there and the sums lose nothing in practice, so the rounded x does
+// not depend on summation order (the same reasoning as the bf16 recurrence).
+#include <math.h>
+
+#include "sb_internal.h"
+#include "bf16_round.h"
+
+namespace sb {
+namespace {
+
+constexpr int AT_THREADS = 256;   // 4 waves
+
+__device__ __forceinline__ double bf_to_d(uint32_t bits16) { return (double)__uint_as_float(bits16 << 16); }
+
+template <int E>
+struct Vec;
+template <>
+struct Vec<1> { typedef uint16_t t; };
+template <>
+struct Vec<2> { typedef uint32_t t; };
+template <>
+struct Vec<4> { typedef unsigned int t __attribute__((ext_vector_type(2))); };
+template <>
+struct Vec<8> { typedef unsigned int t __attribute__((ext_vector_type(4))); };
+
+// E bf16 values (2E bytes) as 16-bit codes.
+template <int E>
+__device__ __forceinline__ void load_bf(const uint16_t *p, uint32_t (&out)[E]) {
+  const typename Vec<E>::t v = *reinterpret_cast<const typename Vec<E>::t *>(p);
+  if constexpr (E == 1) {
+    out[0] = v;
+  } else if constexpr (E == 2) {
+    out[0] = v & 0xFFFFu;
+    out[1] = v >> 16;
+  } else {
+#pragma unroll
+    for (int i = 0; i < E / 2; ++i) {
+      out[2 * i] = v[i] & 0xFFFFu;
+      out[2 * i + 1] = v[i] >> 16;
+    }
+  }
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// d = 256 E. Lane l of wave w owns columns w d/4 + l E .. + E - 1 (the V
+// pass), and for the K pass the four pieces p d/4 + l E .. + E - 1.
+template <int E>
+__global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
+  extern __shared__ double sc[];   // [max_len_cap] scores, then weights
+  __shared__ double red[4];
+  const int R = st.ctrl->R;
+  const int d = st.d, L = st.kv_layers, planes = 2 * L;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int q4 = d / 4;
+  const size_t plane_elems = (size_t)st.max_len_cap * d;
+  const double scale = 1.0 / sqrt((double)d);
+  const uint16_t *hb = static_cast<const uint16_t *>(st.hbuf);
+  uint16_t *xb = static_cast<uint16_t *>(st.xbuf);
+
+  for (int r = blockIdx.x; r < R; r += gridDim.x) {
+    const int slot = st.r_slot[r];
+    const int t = st.r_t[r];                         // positions, the new one included
+    const int b = slot / st.k;
+    const uint16_t *buf = st.b_par[b] ? st.kv1 : st.kv0;
+    const uint16_t *hist = buf + (size_t)slot * planes * plane_elems;
+    const uint16_t *nrow = st.kvnew + (size_t)r * planes * d;
+    // Query (this row's new state), the lane's four K-pass pieces.
+    double q[4][E];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t c[E];
+      load_bf<E>(hb + (size_t)r * d + p * q4 + lane * E, c);
+#pragma unroll
+      for (int e = 0; e < E; ++e) q[p][e] = bf_to_d(c[e]);
+    }
+    double acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.0;
+
+    for (int l = 0; l < L; ++l) {
+      const uint16_t *Kh = hist + (size_t)(2 * l) * plane_elems;
+      const uint16_t *Vh = hist + (size_t)(2 * l + 1) * plane_elems;
+      const uint16_t *Kn = nrow + (size_t)(2 * l) * d;
+      const uint16_t *Vn = nrow + (size_t)(2 * l + 1) * d;
+      // Scores: wave w takes positions s = w, w + 4, ..., four at a time
+      // (their loads issued together; positions past t re-read the last row
+      // and are dropped).
+      double mx = -INFINITY;
+      for (int s0 = w; s0 < t; s0 += 16) {
+        uint32_t c[4][4][E];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int s = min(s0 + 4 * u, t - 1);
+          const uint16_t *row = s < t - 1 ? Kh + (size_t)s * d : Kn;
+#pragma unroll
+          for (int p = 0; p < 4; ++p) load_bf<E>(row + p * q4 + lane * E, c[u][p]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          double part = 0.0;
+#pragma unroll
+          for (int p = 0; p < 4; ++p)
+#pragma unroll
+            for (int e = 0; e < E; ++e) part = fma(q[p][e], bf_to_d(c[u][p][e]), part);
+          const int s = s0 + 4 * u;
+          const double sv = wave_sum_d(part) * scale;
+          if (s < t) {
+            if (lane == 0) sc[s] = sv;
+            mx = fmax(mx, sv);
+          }
+        }
+      }
+      if (lane == 0) red[w] = mx;
+      __syncthreads();
+      const double m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+      __syncthreads();
+      // Weights exp(s - max) and their sum (fixed order: lanes, then waves).
+      double ls = 0.0;
+      for (int s = threadIdx.x; s < t; s += AT_THREADS) {
+        const double ev = exp(sc[s] - m);
+        sc[s] = ev;
+        ls += ev;
+      }
+      ls = wave_sum_d(ls);
+      if (lane == 0) red[w] = ls;
+      __syncthreads();
+      const double den = (red[0] + red[1]) + (red[2] + red[3]);
+      // Read-out over the lane's columns, positions in order.
+      double a[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) a[e] = 0.0;
+      const int col = w * q4 + lane * E;
+#pragma unroll 4
+      for (int s = 0; s < t; ++s) {
+        const uint16_t *row = s < t - 1 ? Vh + (size_t)s * d : Vn;
+        uint32_t c[E];
+        load_bf<E>(row + col, c);
+        const double ws = sc[s];
+#pragma unroll
+        for (int e = 0; e < E; ++e) a[e] = fma(ws, bf_to_d(c[e]), a[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] += a[e] / den;
+      __syncthreads();   // sc and red are rewritten by the next layer
+    }
+    // x = bf16(h + acc / L) over the lane's columns.
+    {
+      const int col = w * q4 + lane * E;
+      uint32_t c[E];
+      load_bf<E>(hb + (size_t)r * d + col, c);
+#pragma unroll
+      for (int e = 0; e < E; ++e) xb[(size_t)r * d + col + e] = bf16_rne_from_double(bf_to_d(c[e]) + acc[e] / (double)L);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn(const DevState &st, hipStream_t s) {
+  const int G = std::min(st.R_max, st.n_cu * 8);
+  const size_t lds = (size_t)st.max_len_cap * sizeof(double);
+  switch (st.d) {
+    case 256: hipLaunchKernelGGL(k_attn<1>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
+    case 512: hipLaunchKernelGGL(k_attn<2>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
+    case 1024: hipLaunchKernelGGL(k_attn<4>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
+    case 2048: hipLaunchKernelGGL(k_attn<8>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sb

@@ -222,7 +222,7 @@ __device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB
   uint32_t boff[NB];
 #pragma unroll
   for (int u = 0; u < NB; ++u) boff[u] = (uint32_t)min(r0 + srow + 32 * u, R - 1) * (uint32_t)rowbytes + scol;
-  const unsigned char *bbase = static_cast<const unsigned char *>(st.hbuf) + (size_t)kbeg * CH;
+  const unsigned char *bbase = static_cast<const unsigned char *>(st.proj_in) + (size_t)kbeg * CH;
   f16v acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f16v{};
@@ -326,7 +326,7 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
   unsigned char (*Bt)[LS] = sm.B[0][g];
   unsigned char (*Bt1)[LS] = sm.B[1][g];
   const uint32_t alane = (uint32_t)lane * 16u;
-  const unsigned char *hb = static_cast<const unsigned char *>(st.hbuf);
+  const unsigned char *hb = static_cast<const unsigned char *>(st.proj_in);
   f16v acc0[NB], acc1[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {

@@ -79,6 +79,9 @@ struct DevState {
   uint16_t *kv0, *kv1; // [n*k][L][2][max_len_cap][d]
   uint16_t *kvnew;     // [R_max][L*2*d]
   uint16_t *wkvT;      // [L*2*d][d]  (transposed W_kv: out-feature major)
+  // attention read-out (attn models): projection input x [R_max][d] bf16
+  void *xbuf;
+  const void *proj_in; // rows the projection reads: xbuf (attn) or hbuf
   // model
   const void *W_h, *E, *W_out;
   // W_out re-laid out tile-contiguous: [S][nk][128 rows][128 bytes], one
@@ -87,6 +90,7 @@ struct DevState {
   unsigned char *wout_t;
   // sizes and parameters
   int32_t n, k, d, V, M, max_len_cap, refill_thr, S, R_max, dtype, kv_layers, max_inputs;
+  int32_t attn;        // 1: projection input = h + layer-mean attention read-out
   int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   int32_t n_cu;        // compute units of the device (persistent launches)
@@ -113,6 +117,7 @@ hipError_t launch_rowmerge(const DevState &st, hipStream_t s);
 hipError_t launch_beam(const DevState &st, hipStream_t s);
 hipError_t launch_kv_append(const DevState &st, hipStream_t s);
 hipError_t launch_kv_gather(const DevState &st, hipStream_t s);
+hipError_t launch_attn(const DevState &st, hipStream_t s);
 hipError_t launch_backtrack(const DevState &st, int q0, int q1, hipStream_t s);
 hipError_t launch_init(const DevState &st, hipStream_t s);
 hipError_t launch_relayout_wout(const DevState &st, hipStream_t s);

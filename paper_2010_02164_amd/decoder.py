@@ -55,10 +55,10 @@ def make_params(k, n, eps, delta, M, sched, max_len_cap, max_inputs, rule=None, 
                       pool=0 if pool is None else int(pool))
 
 
-def make_model(vocab, d, dtype, beta, W_h=0, E=0, W_out=0, kv_layers=0, W_kv=0) -> N.SbModel:
+def make_model(vocab, d, dtype, beta, W_h=0, E=0, W_out=0, kv_layers=0, W_kv=0, attn=False) -> N.SbModel:
     return N.SbModel(vocab=int(vocab), d=int(d), dtype=N.SB_BF16 if dtype == "bf16" else N.SB_F32,
                      eos_beta=float(beta), W_h=W_h or None, E=E or None, W_out=W_out or None,
-                     kv_layers=int(kv_layers), W_kv=W_kv or None)
+                     kv_layers=int(kv_layers), W_kv=W_kv or None, attn=int(bool(attn)))
 
 
 def workspace_bytes(model: N.SbModel, params: N.SbParams) -> int:
@@ -75,7 +75,7 @@ class Decoder:
     def __init__(self, W_h, E, W_out, *, beta: float, k: int, n: int, eps: float = 0.0,
                  delta: Optional[float] = None, M: Optional[int] = None, sched: str = "var_stream",
                  max_len_cap: int = 256, max_inputs: int = 1024, W_kv=None, stream=None,
-                 pool: Optional[int] = None):
+                 pool: Optional[int] = None, attn: bool = False):
         import torch
         self.torch = torch
         if not torch.cuda.is_available():
@@ -91,7 +91,7 @@ class Decoder:
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.model = make_model(V, d, self.dtype, beta, W_h.data_ptr(), E.data_ptr(), W_out.data_ptr(),
                                 0 if W_kv is None else W_kv.shape[0],
-                                0 if W_kv is None else W_kv.data_ptr())
+                                0 if W_kv is None else W_kv.data_ptr(), attn=attn)
         self.params = make_params(k, n, eps, delta, k if M is None else M, sched, max_len_cap, max_inputs,
                                   pool=pool)
         L = N.lib()
@@ -262,6 +262,7 @@ def decoder_for_workload(wl, sched="var_stream", eps=None, n=None, max_inputs=No
     c = wl.cfg
     if sched == "var_cap" and kw.get("pool") is None:
         kw["pool"] = 2 * (c.n if n is None else n)
+    kw.setdefault("attn", c.attn)
     W_h, E, W_out, W_kv = weights if weights is not None else weights_to_device(wl)
     return Decoder(W_h, E, W_out, W_kv=W_kv, beta=c.beta, k=c.k, n=c.n if n is None else n,
                    eps=c.eps if eps is None else eps, delta=c.delta, M=c.M, sched=sched,

@@ -30,6 +30,20 @@ def score_tol(wl):
     return 2e-2 if wl.is_bf16 else 1e-4
 
 
+def tie_tol(wl):
+    """Decision margin below which a mismatching input is excused.
+
+    1e-4 nats covers fp32/bf16 accumulation-order differences of the logits.
+    With the attention read-out, the bf16 projection input x can differ by
+    one bf16 step in an element where a KV row element did (the KV rows are
+    fp32-accumulated bf16 products, at most one bf16 step from the oracle's
+    fp64 value): |x_j| < 2 gives a step of at most 2^-7, and |W_out[v, j]|
+    stays below 0.14 (4.5 standard deviations of N(0, 1/1024)), so a logit
+    moves by at most 1.1e-3 per such element and two candidates' gap by
+    2.2e-3. The threshold for attention workloads is 3e-3."""
+    return 3e-3 if getattr(wl.cfg, "attn", False) else 1e-4
+
+
 def check_parity(wl, sched, eps=None, n=None, inputs=None, oracle_res=None, weights=None,
                  require_stats=True, pool=None):
     """GPU vs oracle on the same inputs; returns the comparison report."""
@@ -38,7 +52,7 @@ def check_parity(wl, sched, eps=None, n=None, inputs=None, oracle_res=None, weig
     g, st, dec = gpu_decode(wl, sched, eps=eps, n=n, inputs=idx, weights=weights, pool=pool)
     dec.close()
     rep = compare(o.hyps, o.min_margin, [[(h.tokens, h.score, h.status) for h in y] for y in g],
-                  inputs=idx, score_tol=score_tol(wl))
+                  inputs=idx, score_tol=score_tol(wl), tie_tol=tie_tol(wl))
     print(f"[parity] {wl.cfg.name} {sched} eps={eps} n={n} pool={pool} N={len(idx)}: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures[:5]
     if require_stats and rep.n_excused == 0:

@@ -18,7 +18,8 @@ def test_exports_every_declared_symbol(native_lib):
 
 
 def _mp(cfg, **over):
-    m = make_model(cfg.V, cfg.d, cfg.dtype, cfg.beta, 1, 1, 1, cfg.kv_layers, 1 if cfg.kv_layers else 0)
+    m = make_model(cfg.V, cfg.d, cfg.dtype, cfg.beta, 1, 1, 1, cfg.kv_layers, 1 if cfg.kv_layers else 0,
+                   attn=cfg.attn)
     p = make_params(cfg.k, cfg.n, cfg.eps, cfg.delta, cfg.M, "var_stream", cfg.max_len_cap, cfg.N)
     for k, v in over.items():
         setattr(m if hasattr(m, k) else p, k, v)
@@ -77,6 +78,26 @@ def test_capacity_pool_workspace(native_lib):
     extra = workspace_bytes(m2, p2) - workspace_bytes(m, p)
     slot_state = c.n * c.k * c.d * 4
     assert slot_state <= extra < 2 * slot_state
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(attn=2), N.SB_E_INVALID_ARG), (dict(d=1536), N.SB_E_UNSUPPORTED),
+])
+def test_validate_rejects_attention(native_lib, over, code):
+    m, p = _mp(CONFIGS[6], **over)
+    assert native_lib.sb_validate(ctypes.byref(m), ctypes.byref(p)) == code
+
+
+def test_attention_needs_kv_state(native_lib):
+    m, p = _mp(CONFIGS[4], attn=1)
+    assert native_lib.sb_validate(ctypes.byref(m), ctypes.byref(p)) == N.SB_E_INVALID_ARG
+
+
+def test_attention_workspace(native_lib):
+    # The attention read-out adds one bf16 row per expanded candidate.
+    m5, p5 = _mp(CONFIGS[5])
+    m6, p6 = _mp(CONFIGS[6])
+    assert workspace_bytes(m6, p6) - workspace_bytes(m5, p5) >= CONFIGS[6].R_max * CONFIGS[6].d * 2
 
 
 def test_delta_inf_is_valid(native_lib):

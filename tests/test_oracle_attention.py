@@ -53,7 +53,7 @@ def test_single_position_reads_its_value_row(seed):
     x = bf16_round(h + np.mean(kv[:, 1], axis=0))
     want = log_softmax(el.logits(x[None, :], np.array([1]), np.array([7])))[0]
     assert np.max(np.abs(lp - want)) < 1e-12
-    assert np.array_equal(st[0], h) and st[1].shape == (3, 1, 16)
+    assert np.array_equal(st[0], h) and att.kv(st)[0].shape == (3, 1, 16)
 
 
 @pytest.mark.parametrize("seed", [0, 3])
@@ -79,17 +79,18 @@ def test_two_positions_logistic_form(seed):
     steps = teacher_forced(att, h0_of(seed), [6, 1])
     (s1, _), (s2, lp) = steps
     h = s2[0]
+    K, V = att.kv(s2)
     acc = np.zeros(16)
     for l in range(3):
-        k0, k1 = s2[1][l, 0], s2[1][l, 1]
-        v0, v1 = s2[2][l, 0], s2[2][l, 1]
+        k0, k1 = K[l, 0], K[l, 1]
+        v0, v1 = V[l, 0], V[l, 1]
         g = 1.0 / (1.0 + math.exp(-float((k0 - k1) @ h) / 4.0))      # sqrt(16) = 4
         acc += v1 + g * (v0 - v1)
     x = bf16_round(h + acc / 3)
     want = log_softmax(el.logits(x[None, :], np.array([2]), np.array([7])))[0]
     assert np.max(np.abs(lp - want)) < 1e-12
     # the KV rows are those of the two states, in order
-    assert np.array_equal(s2[1][:, 0], el.kv_row(s1[0])[:, 0])
+    assert np.array_equal(K[:, 0], el.kv_row(s1[0])[:, 0])
 
 
 def test_recurrence_reads_h_not_the_attention_input():

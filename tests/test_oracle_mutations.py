@@ -87,12 +87,12 @@ MUTATIONS = [
     ("attn_keys_as_values", "decoder", "out += (w / np.sum(w)) @ V[l]", "out += (w / np.sum(w)) @ K[l]",
      ["attn_single", "attn_uniform"]),
     ("attn_layers_summed", "decoder", "return out / self.L", "return out", ["attn_single", "attn_two"]),
-    ("attn_excludes_new_row", "decoder", "self.attention(h[r], K2, V2)", "self.attention(h[r], K, V)",
+    ("attn_excludes_new_row", "decoder", "K, V = self.kv(st)", "K, V = self.kv((h[r], chain))",
      ["attn_single", "attn_two"]),
-    ("attn_state_carries_x", "decoder", "new.append((h[r], K2, V2))", "new.append((x[r], K2, V2))",
+    ("attn_state_carries_x", "decoder", "new.append(st)", "new.append((x[r], st[1]))",
      ["attn_recurrence"]),
-    ("attn_input_not_rounded", "decoder", "x[r] = bf16_round(h[r] + self.attention(h[r], K2, V2))",
-     "x[r] = h[r] + self.attention(h[r], K2, V2)", ["attn_single"]),
+    ("attn_input_not_rounded", "decoder", "x[r] = bf16_round(h[r] + self.attention(h[r], K, V))",
+     "x[r] = h[r] + self.attention(h[r], K, V)", ["attn_single"]),
     ("refill_strict", "search", "len(live) <= eps * P", "len(live) < eps * P", ["fig1", "cap_schedule"]),
     ("refill_against_n", "search", "len(live) <= eps * P", "len(live) <= eps * n", ["cap_schedule"]),
     ("refill_to_n", "search", "m = min(P - len(live), N - c)", "m = min(n - len(live), N - c)",
