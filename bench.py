@@ -198,7 +198,7 @@ def main():
         "config": {"workload": _workload_desc(cfg, args.sched, eps, pool), "key": workload_key, "inputs": N,
                    "parallelism": "single GPU"},
         "expansions_per_s": exps_per_s,
-        "search": {k: st[k] for k in ("timesteps", "expansions", "noops", "refills", "hyps")},
+        "search": {k: st[k] for k in ("timesteps", "expansions", "noops", "refills", "hyps", "positions")},
         "roofline": {"bound": "mfma", "kernel": "k_proj (vocabulary projection + log-sum-exp + top-k)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": measured_traffic(workload_key), "launches": proj_launches,

@@ -147,9 +147,11 @@ typedef struct {
 
 /* Counters of Table 5's columns: timesteps, candidate expansions (decoder
  * evaluations of one active candidate), plus no-op expansions of terminated
- * candidates, refills, admitted inputs, finalized hypotheses, finished inputs. */
+ * candidates, refills, admitted inputs, finalized hypotheses, finished inputs,
+ * and the output positions t of the expansions summed (an attention step
+ * reads t KV rows per layer and plane). */
 typedef struct {
-  int64_t timesteps, expansions, noops, refills, admitted, hyps, finished;
+  int64_t timesteps, expansions, noops, refills, admitted, hyps, finished, positions;
 } sb_stats_t;
 
 typedef struct sb_decoder sb_decoder;

@@ -56,6 +56,7 @@ class SearchResult:
     noops: int = 0
     refills: int = 0
     admitted: int = 0
+    positions: int = 0                  # output positions t of the expanded rows, summed
     rows_per_step: List[int] = dataclasses.field(default_factory=list)
 
     @property
@@ -150,6 +151,7 @@ def decode(decoder, h0: np.ndarray, Lx: Sequence[int], max_len: Sequence[int],
         h_new, lp = decoder.expand(h_prev, y, t, lx)
         res.timesteps += 1
         res.expansions += len(rows)
+        res.positions += int(t.sum())
         res.rows_per_step.append(len(rows))
         if on_step is not None:
             on_step(res.timesteps, [b.input for b in sel], len(rows))

@@ -48,7 +48,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, xbuf, wout_t, total;
+      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, xbuf, attn_part, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -113,7 +113,10 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
     L.kvnew = take(Rm * planes * d * 2);
     L.wkvT = take(planes * d * d * 2);
   }
-  if (m.attn) L.xbuf = take(Rm * d * 2);
+  if (m.attn) {
+    L.xbuf = take(Rm * d * 2);
+    L.attn_part = take(Rm * (size_t)m.kv_layers * d * 8);
+  }
   L.total = off;
   return L;
 }
@@ -342,6 +345,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   }
   st.attn = model->attn;
   st.xbuf = model->attn ? w + L.xbuf : nullptr;
+  st.attn_part = model->attn ? reinterpret_cast<double *>(w + L.attn_part) : nullptr;
   st.proj_in = model->attn ? st.xbuf : st.hbuf;
   st.W_h = model->W_h;
   st.E = model->E;
@@ -578,6 +582,7 @@ sb_status sb_stats(sb_decoder *dec, sb_stats_t *out) {
   out->admitted = c.admitted;
   out->hyps = c.hyps;
   out->finished = c.finished;
+  out->positions = c.positions;
   return SB_OK;
 }
 

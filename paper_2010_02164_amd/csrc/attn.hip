@@ -7,6 +7,10 @@
 // All arithmetic after the bf16 loads is fp64: products of bf16 values are
 // exact there and the sums lose nothing in practice, so the rounded x does
 // not depend on summation order (the same reasoning as the bf16 recurrence).
+//
+// Two kernels: k_attn computes a_l of one (row, layer) per workgroup visit
+// into an fp64 scratch [R][L][d] (so the layers of a row run side by side),
+// k_attn_combine adds the layers in order and rounds x.
 #include <math.h>
 
 #include "sb_internal.h"
@@ -56,6 +60,7 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 
 // d = 256 E. Lane l of wave w owns columns w d/4 + l E .. + E - 1 (the V
 // pass), and for the K pass the four pieces p d/4 + l E .. + E - 1.
+// Persistent over the R*L (row, layer) pairs, layer minor.
 template <int E>
 __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
   extern __shared__ double sc[];   // [max_len_cap] scores, then weights
@@ -67,9 +72,9 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
   const size_t plane_elems = (size_t)st.max_len_cap * d;
   const double scale = 1.0 / sqrt((double)d);
   const uint16_t *hb = static_cast<const uint16_t *>(st.hbuf);
-  uint16_t *xb = static_cast<uint16_t *>(st.xbuf);
 
-  for (int r = blockIdx.x; r < R; r += gridDim.x) {
+  for (int pr = blockIdx.x; pr < R * L; pr += gridDim.x) {
+    const int r = pr / L, l = pr - r * L;
     const int slot = st.r_slot[r];
     const int t = st.r_t[r];                         // positions, the new one included
     const int b = slot / st.k;
@@ -85,11 +90,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
 #pragma unroll
       for (int e = 0; e < E; ++e) q[p][e] = bf_to_d(c[e]);
     }
-    double acc[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = 0.0;
-
-    for (int l = 0; l < L; ++l) {
+    {
       const uint16_t *Kh = hist + (size_t)(2 * l) * plane_elems;
       const uint16_t *Vh = hist + (size_t)(2 * l + 1) * plane_elems;
       const uint16_t *Kn = nrow + (size_t)(2 * l) * d;
@@ -151,25 +152,45 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
 #pragma unroll
         for (int e = 0; e < E; ++e) a[e] = fma(ws, bf_to_d(c[e]), a[e]);
       }
+      double *out = st.attn_part + (size_t)pr * d + col;
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] += a[e] / den;
-      __syncthreads();   // sc and red are rewritten by the next layer
+      for (int e = 0; e < E; ++e) out[e] = a[e] / den;
+      __syncthreads();   // sc and red are rewritten by the next pair
     }
-    // x = bf16(h + acc / L) over the lane's columns.
-    {
-      const int col = w * q4 + lane * E;
-      uint32_t c[E];
-      load_bf<E>(hb + (size_t)r * d + col, c);
+  }
+}
+
+// x[r][j] = bf16(h[r][j] + (a_0 + a_1 + ... + a_{L-1})[j] / L), layers added
+// in order. One thread per 4 columns.
+__global__ __launch_bounds__(AT_THREADS) void k_attn_combine(DevState st) {
+  const int R = st.ctrl->R;
+  const int d = st.d, L = st.kv_layers, nq = d / 4;
+  const uint16_t *hb = static_cast<const uint16_t *>(st.hbuf);
+  uint16_t *xb = static_cast<uint16_t *>(st.xbuf);
+  for (int i = blockIdx.x * AT_THREADS + threadIdx.x; i < R * nq; i += gridDim.x * AT_THREADS) {
+    const int r = i / nq, j = (i - r * nq) * 4;
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int l = 0; l < L; ++l) {
+      const double *p = st.attn_part + ((size_t)r * L + l) * d + j;
 #pragma unroll
-      for (int e = 0; e < E; ++e) xb[(size_t)r * d + col + e] = bf16_rne_from_double(bf_to_d(c[e]) + acc[e] / (double)L);
+      for (int e = 0; e < 4; ++e) s[e] += p[e];
     }
+    uint32_t c[4];
+    load_bf<4>(hb + (size_t)r * d + j, c);
+    unsigned int o[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+      o[e] = (uint32_t)bf16_rne_from_double(bf_to_d(c[2 * e]) + s[2 * e] / (double)L) |
+             ((uint32_t)bf16_rne_from_double(bf_to_d(c[2 * e + 1]) + s[2 * e + 1] / (double)L) << 16);
+    typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+    *reinterpret_cast<u2 *>(xb + (size_t)r * d + j) = u2{o[0], o[1]};
   }
 }
 
 }  // namespace
 
 hipError_t launch_attn(const DevState &st, hipStream_t s) {
-  const int G = std::min(st.R_max, st.n_cu * 8);
+  const int G = std::min(st.R_max * st.kv_layers, st.n_cu * 8);
   const size_t lds = (size_t)st.max_len_cap * sizeof(double);
   switch (st.d) {
     case 256: hipLaunchKernelGGL(k_attn<1>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
@@ -178,6 +199,10 @@ hipError_t launch_attn(const DevState &st, hipStream_t s) {
     case 2048: hipLaunchKernelGGL(k_attn<8>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
     default: return hipErrorInvalidValue;
   }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int G2 = std::min((st.R_max * (st.d / 4) + AT_THREADS - 1) / AT_THREADS, st.n_cu * 4);
+  hipLaunchKernelGGL(k_attn_combine, dim3(G2), dim3(AT_THREADS), 0, s, st);
   return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ struct DevCtrl {
   int32_t n_sel;      // beams selected this step
   int32_t pad0;
   int64_t timesteps, expansions, noops, refills, admitted, hyps, finished;
+  int64_t positions;       // output positions t of the expanded rows, summed
   int64_t rows_hist[64];   // timesteps by rows expanded, bucket = R / hist_width
 };
 
@@ -81,6 +82,7 @@ struct DevState {
   uint16_t *wkvT;      // [L*2*d][d]  (transposed W_kv: out-feature major)
   // attention read-out (attn models): projection input x [R_max][d] bf16
   void *xbuf;
+  double *attn_part;   // [R_max][L][d] per-layer read-outs a_l
   const void *proj_in; // rows the projection reads: xbuf (attn) or hbuf
   // model
   const void *W_h, *E, *W_out;

@@ -286,7 +286,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
 
   // Active and terminated candidates of the selected beams (slot order);
   // each beam's active slots are kept as a bit mask.
-  int act_l = 0, term_l = 0, sel_l = 0;
+  int act_l = 0, term_l = 0, sel_l = 0, pos_l = 0;
   uint32_t amask[SCHED_MAXB];
 #pragma unroll
   for (int u = 0; u < SCHED_MAXB; ++u) {
@@ -300,6 +300,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
         term_l += status == SLOT_EOS || status == SLOT_MAXLEN;
       }
       act_l += __popc(amask[u]);
+      pos_l += __popc(amask[u]) * (stp[u] + 1);
     }
   }
   long long tot2;
@@ -330,8 +331,9 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
       }
     }
   }
-  int nsel;
+  int nsel, npos;
   block_excl_scan(sel_l, sm, &nsel);
+  block_excl_scan(pos_l, sm, &npos);
 
   if (tid == 0) {
     c->cursor = cursor + admit;
@@ -345,6 +347,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
       c->timesteps += 1;
       c->expansions += R;
       c->noops += noops;
+      c->positions += npos;
     }
     if (admit > 0) {
       c->refills += 1;

@@ -56,7 +56,7 @@ def check_parity(wl, sched, eps=None, n=None, inputs=None, oracle_res=None, weig
     print(f"[parity] {wl.cfg.name} {sched} eps={eps} n={n} pool={pool} N={len(idx)}: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures[:5]
     if require_stats and rep.n_excused == 0:
-        for key in ("timesteps", "expansions", "noops", "refills", "admitted"):
+        for key in ("timesteps", "expansions", "noops", "refills", "admitted", "positions"):
             assert st[key] == getattr(o, key), (key, st[key], getattr(o, key))
         assert st["hyps"] == o.n_hyps
         fin = [y[0].finalize_step for y in g]

@@ -94,10 +94,12 @@ def test_attention_needs_kv_state(native_lib):
 
 
 def test_attention_workspace(native_lib):
-    # The attention read-out adds one bf16 row per expanded candidate.
+    # The attention read-out adds per expanded candidate one bf16 row and
+    # an fp64 row per layer.
+    c = CONFIGS[6]
     m5, p5 = _mp(CONFIGS[5])
-    m6, p6 = _mp(CONFIGS[6])
-    assert workspace_bytes(m6, p6) - workspace_bytes(m5, p5) >= CONFIGS[6].R_max * CONFIGS[6].d * 2
+    m6, p6 = _mp(c)
+    assert workspace_bytes(m6, p6) - workspace_bytes(m5, p5) >= c.R_max * c.d * (2 + 8 * c.kv_layers)
 
 
 def test_delta_inf_is_valid(native_lib):
