@@ -47,8 +47,8 @@ constexpr size_t ALIGN = 256;
 
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
-      s_row, s_prow, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, kv0, kv1, kvnew, wkvT, xbuf, attn_part, wout_t, total;
+      s_row, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
+      o_count, o_hyp, o_tok, kvs, anc, wkvT, xbuf, attn_part, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -90,7 +90,6 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.s_tok = take(nk * 4);
   L.s_h = take(nk * d * es);
   L.s_row = take(nk * 4);
-  L.s_prow = take(nk * 4);
   L.bp = take(Q * MLC * bpw * 4);
   L.r_slot = take(Rm * 4);
   L.r_hsrc = take(Rm * 4);
@@ -108,9 +107,8 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.wout_t = take(S * 128 * d * es);
   if (m.kv_layers > 0) {
     const size_t planes = (size_t)m.kv_layers * 2;
-    L.kv0 = take(nk * planes * MLC * d * 2);
-    L.kv1 = take(nk * planes * MLC * d * 2);
-    L.kvnew = take(Rm * planes * d * 2);
+    L.kvs = take(nk * MLC * planes * d * 2);
+    L.anc = take(2 * nk * ((MLC + 3) / 4 * 4));
     L.wkvT = take(planes * d * d * 2);
   }
   if (m.attn) {
@@ -212,7 +210,6 @@ sb_status launch_step(sb_decoder *dec, hipStream_t s, hipEvent_t e0 = nullptr, h
   HIPCHK(launch_proj(st, s));
   if (e1) HIPCHK(hipEventRecord(e1, s));
   HIPCHK(launch_beam(st, s));
-  if (st.kv_layers > 0) HIPCHK(launch_kv_gather(st, s));
   return SB_OK;
 }
 
@@ -322,7 +319,6 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.s_tok = reinterpret_cast<int32_t *>(w + L.s_tok);
   st.s_h = w + L.s_h;
   st.s_row = reinterpret_cast<int32_t *>(w + L.s_row);
-  st.s_prow = reinterpret_cast<int32_t *>(w + L.s_prow);
   st.bp = reinterpret_cast<uint32_t *>(w + L.bp);
   st.r_slot = reinterpret_cast<int32_t *>(w + L.r_slot);
   st.r_hsrc = reinterpret_cast<int32_t *>(w + L.r_hsrc);
@@ -338,11 +334,11 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.o_hyp = reinterpret_cast<OutHyp *>(w + L.o_hyp);
   st.o_tok = reinterpret_cast<int32_t *>(w + L.o_tok);
   if (model->kv_layers > 0) {
-    st.kv0 = reinterpret_cast<uint16_t *>(w + L.kv0);
-    st.kv1 = reinterpret_cast<uint16_t *>(w + L.kv1);
-    st.kvnew = reinterpret_cast<uint16_t *>(w + L.kvnew);
+    st.kvs = reinterpret_cast<uint16_t *>(w + L.kvs);
+    st.anc = reinterpret_cast<uint8_t *>(w + L.anc);
     st.wkvT = reinterpret_cast<uint16_t *>(w + L.wkvT);
   }
+  st.anc_stride = (dec->params.max_len_cap + 3) / 4 * 4;
   st.attn = model->attn;
   st.xbuf = model->attn ? w + L.xbuf : nullptr;
   st.attn_part = model->attn ? reinterpret_cast<double *>(w + L.attn_part) : nullptr;
@@ -684,15 +680,26 @@ sb_status sb_debug_slot(sb_decoder *dec, int32_t beam, int32_t rank, int32_t *st
   *n_tokens = (int32_t)rev.size();
   if (tokens)
     for (int i = 0; i < (int)rev.size() && i < tok_cap; ++i) tokens[i] = rev[rev.size() - 1 - i];
-  if (kv && st.kv_layers > 0 && sst == SLOT_ACTIVE) {
+  if (kv && st.kv_layers > 0 && sst == SLOT_ACTIVE && bst > 0) {
+    // Rows of levels 0 .. steps-1, found through the slot's ancestor ranks.
     const int planes = st.kv_layers * 2;
-    const size_t plane_elems = (size_t)st.max_len_cap * st.d;
-    const uint16_t *buf = bpar ? st.kv1 : st.kv0;
+    std::vector<uint8_t> anc((size_t)bst);
+    HIPCHK(hipMemcpyAsync(anc.data(), st.anc + ((size_t)bpar * st.n * st.k + slot) * st.anc_stride, (size_t)bst,
+                          hipMemcpyDeviceToHost, dec->stream));
+    HIPCHK(hipStreamSynchronize(dec->stream));
+    for (int lev = 0; lev < bst; ++lev)
+      if (anc[lev] >= st.k) {
+        dec->err = "sb_debug_slot: corrupt KV ancestry";
+        return SB_E_STATE;
+      }
     for (int pl = 0; pl < planes; ++pl) {
       const int64_t need = (int64_t)(pl + 1) * bst * st.d;
       if (need > kv_cap) break;
-      HIPCHK(hipMemcpyAsync(kv + (size_t)pl * bst * st.d, buf + ((size_t)slot * planes + pl) * plane_elems,
-                            (size_t)bst * st.d * 2, hipMemcpyDeviceToHost, dec->stream));
+      for (int lev = 0; lev < bst; ++lev) {
+        const size_t src = ((((size_t)beam * st.max_len_cap + lev) * st.k + anc[lev]) * planes + pl) * st.d;
+        HIPCHK(hipMemcpyAsync(kv + ((size_t)pl * bst + lev) * st.d, st.kvs + src, (size_t)st.d * 2,
+                              hipMemcpyDeviceToHost, dec->stream));
+      }
     }
     HIPCHK(hipStreamSynchronize(dec->stream));
   }

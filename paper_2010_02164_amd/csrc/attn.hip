@@ -1,8 +1,9 @@
 // Length-dependent decoder step: the projection input of a row is
 // x = bf16(h + (1/L) sum_l a_l), a_l = sum_s softmax_s(K_l[s] . h / sqrt(d)) V_l[s]
-// over the candidate's own KV rows s = 0 .. t-1 (its history in the slot's
-// KV buffer, the current step's row in kvnew). This is the self-attention
-// whose cost grows with the output position (App. A.2, Fig. 2).
+// over the candidate's own KV rows s = 0 .. t-1 (row s is stored at
+// (beam, s, rank of its ancestor at level s); the current step's row at the
+// candidate's own rank). This is the self-attention whose cost grows with
+// the output position (App. A.2, Fig. 2).
 //
 // All arithmetic after the bf16 loads is fp64: products of bf16 values are
 // exact there and the sums lose nothing in practice, so the rounded x does
@@ -63,24 +64,28 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 // Persistent over the R*L (row, layer) pairs, layer minor.
 template <int E>
 __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
-  extern __shared__ double sc[];   // [max_len_cap] scores, then weights
+  extern __shared__ double sc[];   // [max_len_cap] scores, then weights; then the ranks
   __shared__ double red[4];
   const int R = st.ctrl->R;
-  const int d = st.d, L = st.kv_layers, planes = 2 * L;
+  const int d = st.d, L = st.kv_layers, planes = 2 * L, k = st.k;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int q4 = d / 4;
-  const size_t plane_elems = (size_t)st.max_len_cap * d;
   const double scale = 1.0 / sqrt((double)d);
+  uint8_t *arank = reinterpret_cast<uint8_t *>(sc + st.max_len_cap);   // [max_len_cap]
   const uint16_t *hb = static_cast<const uint16_t *>(st.hbuf);
 
   for (int pr = blockIdx.x; pr < R * L; pr += gridDim.x) {
     const int r = pr / L, l = pr - r * L;
     const int slot = st.r_slot[r];
     const int t = st.r_t[r];                         // positions, the new one included
-    const int b = slot / st.k;
-    const uint16_t *buf = st.b_par[b] ? st.kv1 : st.kv0;
-    const uint16_t *hist = buf + (size_t)slot * planes * plane_elems;
-    const uint16_t *nrow = st.kvnew + (size_t)r * planes * d;
+    const int b = slot / k;
+    // Rank of the candidate whose expansion wrote position s: its ancestors'
+    // (current ancestry buffer of the beam), then its own.
+    const uint8_t *an = st.anc + ((size_t)st.b_par[b] * st.n * k + slot) * st.anc_stride;
+    for (int s = threadIdx.x; s < t - 1; s += AT_THREADS) arank[s] = (uint8_t)min((int)an[s], k - 1);
+    if (threadIdx.x == 0) arank[t - 1] = (uint8_t)(slot - b * k);
+    __syncthreads();
+    const uint16_t *kvb = st.kvs + (size_t)b * st.max_len_cap * k * planes * d;
     // Query (this row's new state), the lane's four K-pass pieces.
     double q[4][E];
 #pragma unroll
@@ -91,10 +96,10 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
       for (int e = 0; e < E; ++e) q[p][e] = bf_to_d(c[e]);
     }
     {
-      const uint16_t *Kh = hist + (size_t)(2 * l) * plane_elems;
-      const uint16_t *Vh = hist + (size_t)(2 * l + 1) * plane_elems;
-      const uint16_t *Kn = nrow + (size_t)(2 * l) * d;
-      const uint16_t *Vn = nrow + (size_t)(2 * l + 1) * d;
+      // Row of position s in plane j of this layer.
+      auto row_of = [&](int s, int j) {
+        return kvb + (((size_t)s * k + arank[s]) * planes + 2 * l + j) * d;
+      };
       // Scores: wave w takes positions s = w, w + 4, ..., four at a time
       // (their loads issued together; positions past t re-read the last row
       // and are dropped).
@@ -103,8 +108,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
         uint32_t c[4][4][E];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int s = min(s0 + 4 * u, t - 1);
-          const uint16_t *row = s < t - 1 ? Kh + (size_t)s * d : Kn;
+          const uint16_t *row = row_of(min(s0 + 4 * u, t - 1), 0);
 #pragma unroll
           for (int p = 0; p < 4; ++p) load_bf<E>(row + p * q4 + lane * E, c[u][p]);
         }
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
       const int col = w * q4 + lane * E;
 #pragma unroll 4
       for (int s = 0; s < t; ++s) {
-        const uint16_t *row = s < t - 1 ? Vh + (size_t)s * d : Vn;
+        const uint16_t *row = row_of(s, 1);
         uint32_t c[E];
         load_bf<E>(row + col, c);
         const double ws = sc[s];
@@ -155,7 +159,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
       double *out = st.attn_part + (size_t)pr * d + col;
 #pragma unroll
       for (int e = 0; e < E; ++e) out[e] = a[e] / den;
-      __syncthreads();   // sc and red are rewritten by the next pair
+      __syncthreads();   // sc, red and arank are rewritten by the next pair
     }
   }
 }
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn_combine(DevState st) {
 
 hipError_t launch_attn(const DevState &st, hipStream_t s) {
   const int G = std::min(st.R_max * st.kv_layers, st.n_cu * 8);
-  const size_t lds = (size_t)st.max_len_cap * sizeof(double);
+  const size_t lds = (size_t)st.max_len_cap * (sizeof(double) + 1);
   switch (st.d) {
     case 256: hipLaunchKernelGGL(k_attn<1>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
     case 512: hipLaunchKernelGGL(k_attn<2>, dim3(G), dim3(AT_THREADS), lds, s, st); break;

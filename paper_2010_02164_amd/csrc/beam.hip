@@ -194,6 +194,9 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     my_ml = st.b_ml[b];
     my_nout = st.b_nout[b];
   }
+  // The KV ancestry buffer holding this beam's current ranks (read before
+  // thread 0 flips the parity at the end of the step).
+  const int apar = st.kv_layers > 0 ? st.b_par[b] : 0;
   // b_sel is cleared for every beam when nothing is live (R == 0).
   if (!st.b_sel[b]) return;
   __shared__ int sl_status[KMAX_SUPPORTED], sl_row[KMAX_SUPPORTED];
@@ -425,7 +428,6 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     }
     if (tid < k) {
       st.s_status[base + tid] = SLOT_EMPTY;
-      st.s_prow[base + tid] = -1;
     }
     if (tid == 0) {
       st.o_count[q_in] = total;
@@ -444,10 +446,8 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
       st.s_status[base + tid] = nstat[tid];
       st.s_score[base + tid] = nscore[tid];
       if (ntok[tid] >= 0) st.s_tok[base + tid] = ntok[tid];
-      st.s_prow[base + tid] = nstat[tid] == SLOT_ACTIVE ? sl_row[par] : -1;
     } else {
       st.s_status[base + tid] = SLOT_EMPTY;
-      st.s_prow[base + tid] = -1;
     }
   }
   if (tid == 0) {
@@ -465,6 +465,22 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   for (int x = tid; x < total; x += BEAM_THREADS) {
     const int r = x / chunks, c = x - r * chunks;
     if (nstat[r] == SLOT_ACTIVE) sh[(size_t)(base + r) * chunks + c] = hb[(size_t)sl_row[npar[r]] * chunks + c];
+  }
+  // KV state: an active child's ancestors are its parent's (levels 0 .. t-2)
+  // and the parent itself (level t-1), copied into the other buffer as
+  // 4-byte words; the word holding level t-1 is built by one thread.
+  if (st.kv_layers > 0) {
+    const int A4 = st.anc_stride / 4;
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(st.anc) + ((size_t)apar * st.n * k + base) * A4;
+    uint32_t *dst = reinterpret_cast<uint32_t *>(st.anc) + ((size_t)(apar ^ 1) * st.n * k + base) * A4;
+    const int nw = (t - 1) / 4 + 1, last = (t - 1) / 4, sh8 = ((t - 1) & 3) * 8;
+    for (int x = tid; x < w * nw; x += BEAM_THREADS) {
+      const int r = x / nw, wi = x - r * nw;
+      if (nstat[r] != SLOT_ACTIVE) continue;
+      uint32_t v = src[(size_t)npar[r] * A4 + wi];
+      if (wi == last) v = (v & ~(0xFFu << sh8)) | ((uint32_t)npar[r] << sh8);
+      dst[(size_t)r * A4 + wi] = v;
+    }
   }
 }
 

@@ -1,10 +1,12 @@
 // Per-candidate KV-like state: every expansion appends the rows
 // bf16(h . W_kv[l][j]) (l < L layers, j in {K, V}) at position l_t - 1, and
-// every beam update hands each surviving active candidate a copy of its
-// parent's rows (the reorder of incremental decoder state that the paper's
-// transformer decoder performs, App. A.2). State lives in two buffers; a
-// beam's rows move to the other buffer at each of its steps, so a parent's
-// rows are never overwritten while a child still needs them.
+// every beam update hands each surviving active candidate its parent's rows
+// (the reorder of incremental decoder state that the paper's transformer
+// decoder performs, App. A.2). The rows are not copied: the row of an
+// expansion is stored once, at (beam, level, rank) of the expanded
+// candidate, and a candidate reaches its rows through the ranks of its
+// ancestors per level, which the beam update passes on (a few bytes per
+// child instead of 2 L d t bytes).
 #include "sb_internal.h"
 
 namespace sb {
@@ -29,7 +31,9 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
   return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
-// kvnew[r][o] = bf16(sum_i h[r][i] * W_kvT[o][i]), o over L*2*d outputs.
+// kvs[beam][t-1][rank][o] = bf16(sum_i h[r][i] * W_kvT[o][i]) for row r
+// (the candidate at rank `rank` of the beam, emitting position t), o over
+// the L*2*d outputs.
 __global__ __launch_bounds__(THREADS, 2) void k_kv_append(DevState st) {
   const int R = st.ctrl->R;
   const int d = st.d, NO = st.kv_layers * 2 * d;
@@ -85,7 +89,8 @@ __global__ __launch_bounds__(THREADS, 2) void k_kv_append(DevState st) {
   }
   const int j = r0 + wb * 32 + (lane & 31);
   if (j >= R) return;
-  uint16_t *out = st.kvnew + (size_t)j * NO;
+  const int slot = st.r_slot[j], beam = slot / st.k, rank = slot - beam * st.k;
+  uint16_t *out = st.kvs + (((size_t)beam * st.max_len_cap + (st.r_t[j] - 1)) * st.k + rank) * NO;
 #pragma unroll
   for (int vb = 0; vb < 2; ++vb) {
     const f16v &acc = vb ? acc1 : acc0;
@@ -98,34 +103,6 @@ __global__ __launch_bounds__(THREADS, 2) void k_kv_append(DevState st) {
       *reinterpret_cast<u2 *>(out + o) = pk;
     }
   }
-}
-
-// One workgroup per (slot, plane): if the slot holds an active candidate
-// created this step, copy its parent's rows 0..t-2 from the old buffer and
-// write row t-1 from kvnew of the parent's row.
-__global__ __launch_bounds__(THREADS) void k_kv_gather(DevState st) {
-  if (st.ctrl->R == 0) return;
-  const int planes = st.kv_layers * 2;
-  const int slot = blockIdx.x / planes;
-  const int plane = blockIdx.x - slot * planes;
-  const int b = slot / st.k;
-  if (!st.b_sel[b] || st.b_input[b] < 0) return;   // not stepped, or finished
-  const int prow = st.s_prow[slot];
-  if (prow < 0) return;
-  const int src_slot = st.r_slot[prow];
-  const int t = st.b_steps[b];                     // rows after this step
-  const int par = st.b_par[b];                     // buffer holding the new rows
-  uint16_t *dstbuf = par ? st.kv1 : st.kv0;
-  const uint16_t *srcbuf = par ? st.kv0 : st.kv1;
-  const size_t plane_elems = (size_t)st.max_len_cap * st.d;
-  const size_t slot_elems = plane_elems * planes;
-  const u4 *src = reinterpret_cast<const u4 *>(srcbuf + src_slot * slot_elems + plane * plane_elems);
-  u4 *dst = reinterpret_cast<u4 *>(dstbuf + (size_t)slot * slot_elems + plane * plane_elems);
-  const int row_chunks = st.d / 8;                 // 16-byte chunks per row
-  const int copy_chunks = (t - 1) * row_chunks;
-  for (int c = threadIdx.x; c < copy_chunks; c += THREADS) dst[c] = src[c];
-  const u4 *nw = reinterpret_cast<const u4 *>(st.kvnew + (size_t)prow * planes * st.d + (size_t)plane * st.d);
-  for (int c = threadIdx.x; c < row_chunks; c += THREADS) dst[copy_chunks + c] = nw[c];
 }
 
 __global__ void k_transpose(const uint16_t *W, uint16_t *WT, int L2, int d) {
@@ -145,12 +122,6 @@ hipError_t launch_kv_append(const DevState &st, hipStream_t s) {
   const int NO = st.kv_layers * 2 * st.d;
   const int G = (NO / BV) * ((st.R_max + BR - 1) / BR);
   hipLaunchKernelGGL(k_kv_append, dim3(G), dim3(THREADS), 0, s, st);
-  return hipGetLastError();
-}
-
-hipError_t launch_kv_gather(const DevState &st, hipStream_t s) {
-  const int G = st.n * st.k * st.kv_layers * 2;
-  hipLaunchKernelGGL(k_kv_gather, dim3(G), dim3(THREADS), 0, s, st);
   return hipGetLastError();
 }
 

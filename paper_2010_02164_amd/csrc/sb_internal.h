@@ -59,7 +59,6 @@ struct DevState {
   int32_t *s_tok;      // last token (0 for a fresh beam: the start symbol)
   void *s_h;           // [n*k][d] state after consuming the candidate's tokens
   int32_t *s_row;      // row of the slot this step, -1 if not expanded
-  int32_t *s_prow;     // for the KV gather: row of the new candidate's parent, -1 if none
   uint32_t *bp;        // [max_inputs][max_len_cap][bpw] backpointers, by queue position
   // rows [R_max]: per-row metadata written by the scheduler
   int32_t *r_slot;     // slot of the expanded candidate
@@ -76,9 +75,12 @@ struct DevState {
   int32_t *o_count;    // [max_inputs] |Y[i]| (0 = unfinished)
   OutHyp *o_hyp;       // [max_inputs][k]
   int32_t *o_tok;      // [max_inputs][k][max_len_cap]
-  // KV-like state (bf16 bits)
-  uint16_t *kv0, *kv1; // [n*k][L][2][max_len_cap][d]
-  uint16_t *kvnew;     // [R_max][L*2*d]
+  // KV-like state (bf16 bits). The row produced by expanding the candidate
+  // at (beam, level, rank) is stored once, at kvs[beam][level][rank]; a
+  // candidate's rows are those of its ancestors, whose ranks per level it
+  // keeps in anc (two buffers, the beam's parity picks the current one).
+  uint16_t *kvs;       // [n][max_len_cap][k][L*2][d]
+  uint8_t *anc;        // [2][n*k][anc_stride]: rank of the ancestor at each level
   uint16_t *wkvT;      // [L*2*d][d]  (transposed W_kv: out-feature major)
   // attention read-out (attn models): projection input x [R_max][d] bf16
   void *xbuf;
@@ -93,6 +95,7 @@ struct DevState {
   // sizes and parameters
   int32_t n, k, d, V, M, max_len_cap, refill_thr, S, R_max, dtype, kv_layers, max_inputs;
   int32_t attn;        // 1: projection input = h + layer-mean attention read-out
+  int32_t anc_stride;  // bytes per slot of anc: max_len_cap rounded up to 4
   int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   int32_t n_cu;        // compute units of the device (persistent launches)
@@ -118,7 +121,6 @@ hipError_t launch_proj(const DevState &st, hipStream_t s);
 hipError_t launch_rowmerge(const DevState &st, hipStream_t s);
 hipError_t launch_beam(const DevState &st, hipStream_t s);
 hipError_t launch_kv_append(const DevState &st, hipStream_t s);
-hipError_t launch_kv_gather(const DevState &st, hipStream_t s);
 hipError_t launch_attn(const DevState &st, hipStream_t s);
 hipError_t launch_backtrack(const DevState &st, int q0, int q1, hipStream_t s);
 hipError_t launch_init(const DevState &st, hipStream_t s);

@@ -369,7 +369,6 @@ __global__ void k_init(DevState st) {
   if (i < st.n * st.k) {
     st.s_status[i] = SLOT_EMPTY;
     st.s_row[i] = -1;
-    st.s_prow[i] = -1;
   }
   if (i < st.max_inputs) st.o_count[i] = 0;
   if (i == 0) {
