@@ -148,10 +148,12 @@ typedef struct {
 /* Counters of Table 5's columns: timesteps, candidate expansions (decoder
  * evaluations of one active candidate), plus no-op expansions of terminated
  * candidates, refills, admitted inputs, finalized hypotheses, finished inputs,
- * and the output positions t of the expansions summed (an attention step
- * reads t KV rows per layer and plane). */
+ * the output positions t of the expansions summed (an attention step reads t
+ * KV rows per layer and plane), and the (row, 128-token tile) pairs whose
+ * logits the row merge recomputed because the projection's short per-tile
+ * list could not rule out more of the row's best k there. */
 typedef struct {
-  int64_t timesteps, expansions, noops, refills, admitted, hyps, finished, positions;
+  int64_t timesteps, expansions, noops, refills, admitted, hyps, finished, positions, tile_recomputes;
 } sb_stats_t;
 
 typedef struct sb_decoder sb_decoder;

@@ -46,7 +46,7 @@ class SbHyp(ctypes.Structure):
 class SbStats(ctypes.Structure):
     _fields_ = [("timesteps", c_int64), ("expansions", c_int64), ("noops", c_int64),
                 ("refills", c_int64), ("admitted", c_int64), ("hyps", c_int64), ("finished", c_int64),
-                ("positions", c_int64)]
+                ("positions", c_int64), ("tile_recomputes", c_int64)]
 
 
 class StreambeamError(RuntimeError):

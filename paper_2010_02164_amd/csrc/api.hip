@@ -55,6 +55,14 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int kbucket_of(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
 
+// Keys per partial record: the short list when the vocabulary spans at
+// least 64 projection tiles (a tile then rarely holds 4 of a row's best k,
+// and the row merge recomputes the ones that do), else the k-bucket.
+int tile_keys_of(const sb_model &m, const sb_params &p) {
+  const int kb = kbucket_of(p.k + (p.finalize_rule == SB_RULE_FAIRSEQ ? 1 : 0));
+  return proj_tiles(m.vocab) >= 64 ? TILE_KEYS_SHORT : kb;
+}
+
 // Beam records held by the decoder: the cached pool (0 means n).
 int pool_of(const sb_params &p) { return p.pool > 0 ? p.pool : p.n; }
 
@@ -65,7 +73,6 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   // per-row buffers by the n*k rows a timestep may expand.
   const size_t n = pool_of(p), k = p.k, d = m.d, nk = n * k, Rm = (size_t)p.n * k;
   const size_t S = proj_tiles(m.vocab);
-  const size_t KB = kbucket_of(p.k + (p.finalize_rule == SB_RULE_FAIRSEQ ? 1 : 0));
   const size_t bpw = p.finalize_rule == SB_RULE_FAIRSEQ ? 2 * (size_t)p.k : (size_t)p.k;
   const size_t Q = p.max_inputs, MLC = p.max_len_cap;
   size_t off = 0;
@@ -98,7 +105,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.r_Lx = take(Rm * 4);
   L.r_lse = take(Rm * 8);
   L.hbuf = take(Rm * d * es);
-  L.part = take(Rm * S * part_width((int)KB) * 4);
+  L.part = take(Rm * S * part_width(tile_keys_of(m, p)) * 4);
   L.top_lp = take(Rm * k * 8);
   L.top_tok = take(Rm * k * 4);
   L.o_count = take(Q * 4);
@@ -363,6 +370,7 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.rule = p.finalize_rule;
   st.bpw = p.finalize_rule == SB_RULE_FAIRSEQ ? 2 * p.k : p.k;
   st.kbucket = kbucket_of(p.k + st.rule);   // the Fairseq rule draws k+1 children per parent
+  st.tile_keys = tile_keys_of(*model, p);
   st.hist_width = std::max(16, (st.R_max + 63) / 64);
   st.select_all = p.sched == SB_VAR_FIFO ? 1 : 0;
   st.cap = p.sched == SB_VAR_CAP ? 1 : 0;
@@ -579,6 +587,7 @@ sb_status sb_stats(sb_decoder *dec, sb_stats_t *out) {
   out->hyps = c.hyps;
   out->finished = c.finished;
   out->positions = c.positions;
+  out->tile_recomputes = c.tile_recomputes;
   return SB_OK;
 }
 

@@ -61,6 +61,38 @@ __device__ __forceinline__ void wave_lse(float &m, float &s) {
   lse_stage<5>(m, s);
 }
 
+// Logit z[v] of one row recomputed from W_out and the row's projection
+// input (fp32 accumulation), with the EOS bias of token 0.
+__device__ __forceinline__ float recompute_logit(const DevState &st, int row, int v) {
+  const int d = st.d;
+  float z = 0.0f;
+  if (st.dtype == 1) {
+    const uint4 *w = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(st.W_out) + (size_t)v * d);
+    const uint4 *x = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(st.proj_in) + (size_t)row * d);
+    for (int c = 0; c < d / 8; ++c) {
+      const uint4 a = w[c], b = x[c];
+      const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        z = fmaf(__uint_as_float(aw[e] << 16), __uint_as_float(bw[e] << 16), z);
+        z = fmaf(__uint_as_float(aw[e] & 0xFFFF0000u), __uint_as_float(bw[e] & 0xFFFF0000u), z);
+      }
+    }
+  } else {
+    const float4 *w = reinterpret_cast<const float4 *>(static_cast<const float *>(st.W_out) + (size_t)v * d);
+    const float4 *x = reinterpret_cast<const float4 *>(static_cast<const float *>(st.proj_in) + (size_t)row * d);
+    for (int c = 0; c < d / 4; ++c) {
+      const float4 a = w[c], b = x[c];
+      z = fmaf(a.x, b.x, z);
+      z = fmaf(a.y, b.y, z);
+      z = fmaf(a.z, b.z, z);
+      z = fmaf(a.w, b.w, z);
+    }
+  }
+  if (v == 0) z += st.beta * (float)(st.r_t[row] - st.r_Lx[row]);
+  return z;
+}
+
 // Merge the per-tile partials of one row (one wave). Each lane folds the
 // tiles lane, lane+64, ... into (max, sum exp) and a sorted best-KB list
 // (loads issued a batch at a time before they are folded). The row's
@@ -68,14 +100,23 @@ __device__ __forceinline__ void wave_lse(float &m, float &s) {
 // best keys are drawn in k rounds of a wave maximum over the lists' heads,
 // the lane holding the winner dropping it (keys are distinct: they carry
 // the token). Lane r < k receives the key of rank r.
-template <int KB>
+//
+// A tile record keeps its TK best keys (TK <= KB). If a tile's last kept
+// key ranks above the k-th key drawn, the tile may hold further keys of the
+// best k: such tiles (rare: TK of the row's best k - 1 in one
+// 128-token tile) are recomputed from W_out, all their logits enter the
+// lists in place of the record's keys, and the k keys are drawn again. Any
+// other tile's unkept keys rank below its last kept key, so at most at the
+// k-th key drawn, and adding candidates can only raise the k-th key.
+template <int KB, int TK>
 __device__ __forceinline__ double merge_row(const DevState &st, int row, int lane, int k, cand_key &mine) {
-  constexpr int PW = part_width(KB);
-  constexpr int NBT = KB <= 8 ? 4 : 2;   // partials in flight per lane
+  constexpr int PW = part_width(TK);
+  constexpr int NBT = 4;   // partials in flight per lane
   const float *base = st.part + (size_t)row * st.S * PW;
   float m = -INFINITY, s = 0.0f;
   TopK<KB> tk;
   topk_init(tk);
+  cand_key last_max = 0ull;   // largest last kept key over the lane's tiles
 #pragma unroll 1
   for (int t0 = lane; t0 < st.S; t0 += 64 * NBT) {
     float rec[NBT][PW];
@@ -95,14 +136,67 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
 #pragma unroll
     for (int u = 0; u < NBT; ++u) {
       if (t0 + 64 * u < st.S) {
+        TopK<TK> t4;
+        topk_load(t4, rec[u] + 2);
         TopK<KB> o;
-        topk_load(o, rec[u] + 2);
+        topk_init(o);
+#pragma unroll
+        for (int j = 0; j < TK; ++j) o.k[j] = t4.k[j];
         lse_merge(m, s, rec[u][0], rec[u][1]);
+        last_max = t4.k[TK - 1] > last_max ? t4.k[TK - 1] : last_max;
         topk_merge(tk, o);
       }
     }
   }
   wave_lse(m, s);
+  cand_key kth = 0ull;
+  mine = 0ull;
+#pragma unroll 1
+  for (int r = 0; r < k; ++r) {
+    const cand_key best = wave_max_key(tk.k[0]);
+    if (lane == r) mine = best;
+    kth = best;
+    if (tk.k[0] == best) {
+#pragma unroll
+      for (int j = 0; j + 1 < KB; ++j) tk.k[j] = tk.k[j + 1];
+      tk.k[KB - 1] = 0ull;
+    }
+  }
+  if (__ballot(last_max > kth) == 0ull) return (double)m + log((double)s);
+
+  // Rare path: rebuild the lists with the saturated tiles recomputed.
+  topk_init(tk);
+  for (int t0 = 0; t0 < st.S; t0 += 64) {
+    const int t = t0 + lane;
+    bool sat = false;
+    if (t < st.S) {
+      const float *p = base + (size_t)t * PW;
+      TopK<TK> o;
+      topk_load(o, p + 2);
+      sat = o.k[TK - 1] > kth;
+      if (!sat) {
+        TopK<KB> oo;
+        topk_init(oo);
+#pragma unroll
+        for (int j = 0; j < TK; ++j) oo.k[j] = o.k[j];
+        topk_merge(tk, oo);
+      }
+    }
+    unsigned long long mask = __ballot(sat);
+    if (lane == 0 && mask)
+      atomicAdd(reinterpret_cast<unsigned long long *>(&st.ctrl->tile_recomputes),
+                (unsigned long long)__popcll(mask));
+    while (mask) {
+      const int src = __ffsll((long long)mask) - 1;
+      mask &= mask - 1;
+      const int vt = t0 + src;
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int v = vt * 128 + 64 * half + lane;
+        if (v < st.V) topk_insert(tk, make_key(recompute_logit(st, row, v), v));
+      }
+    }
+  }
   mine = 0ull;
 #pragma unroll 1
   for (int r = 0; r < k; ++r) {
@@ -119,7 +213,7 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
 
 // Row merge as its own kernel (wave per row), for the single-expansion
 // debug entry point: writes lse and the k best log-probabilities/tokens.
-template <int KB>
+template <int KB, int TK>
 __global__ __launch_bounds__(256) void k_rowmerge(DevState st) {
   const int R = st.ctrl->R;
   const int lane = threadIdx.x & 63;
@@ -127,7 +221,7 @@ __global__ __launch_bounds__(256) void k_rowmerge(DevState st) {
   if (row >= R) return;
   cand_key mine;
   const int k = st.k;
-  const double lse = merge_row<KB>(st, row, lane, k, mine);
+  const double lse = merge_row<KB, TK>(st, row, lane, k, mine);
   if (lane == 0) st.r_lse[row] = lse;
   if (lane < k) {
     st.top_lp[(size_t)row * k + lane] = (double)key_val(mine) - lse;
@@ -169,7 +263,7 @@ __device__ __forceinline__ void wave_best(double &bs, int &bk) {
   best_stage<5>(bs, bk);
 }
 
-template <int KB>
+template <int KB, int TK>
 __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -228,7 +322,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   for (int par = wave; par < k; par += BEAM_WAVES) {
     if (sl_status[par] != SLOT_ACTIVE) continue;
     cand_key mine;
-    const double lse = merge_row<KB>(st, sl_row[par], lane, KC, mine);
+    const double lse = merge_row<KB, TK>(st, sl_row[par], lane, KC, mine);
     if (lane < KC) {
       ch_lp[par * KC + lane] = (double)key_val(mine) - lse;
       ch_tok[par * KC + lane] = key_idx(mine);
@@ -520,19 +614,33 @@ __global__ __launch_bounds__(256) void k_backtrack(DevState st, int q0, int q1) 
 
 hipError_t launch_rowmerge(const DevState &st, hipStream_t s) {
   const int G = (st.R_max + 3) / 4;
+  const bool sh = st.tile_keys == TILE_KEYS_SHORT;
   switch (st.kbucket) {
-    case 4: hipLaunchKernelGGL((k_rowmerge<4>), dim3(G), dim3(256), 0, s, st); break;
-    case 8: hipLaunchKernelGGL((k_rowmerge<8>), dim3(G), dim3(256), 0, s, st); break;
-    default: hipLaunchKernelGGL((k_rowmerge<16>), dim3(G), dim3(256), 0, s, st); break;
+    case 4: hipLaunchKernelGGL((k_rowmerge<4, 4>), dim3(G), dim3(256), 0, s, st); break;
+    case 8:
+      if (sh) hipLaunchKernelGGL((k_rowmerge<8, 4>), dim3(G), dim3(256), 0, s, st);
+      else hipLaunchKernelGGL((k_rowmerge<8, 8>), dim3(G), dim3(256), 0, s, st);
+      break;
+    default:
+      if (sh) hipLaunchKernelGGL((k_rowmerge<16, 4>), dim3(G), dim3(256), 0, s, st);
+      else hipLaunchKernelGGL((k_rowmerge<16, 16>), dim3(G), dim3(256), 0, s, st);
+      break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_beam(const DevState &st, hipStream_t s) {
+  const bool sh = st.tile_keys == TILE_KEYS_SHORT;
   switch (st.kbucket) {
-    case 4: hipLaunchKernelGGL((k_beam<4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
-    case 8: hipLaunchKernelGGL((k_beam<8>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
-    default: hipLaunchKernelGGL((k_beam<16>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
+    case 4: hipLaunchKernelGGL((k_beam<4, 4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
+    case 8:
+      if (sh) hipLaunchKernelGGL((k_beam<8, 4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+      else hipLaunchKernelGGL((k_beam<8, 8>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+      break;
+    default:
+      if (sh) hipLaunchKernelGGL((k_beam<16, 4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+      else hipLaunchKernelGGL((k_beam<16, 16>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+      break;
   }
   return hipGetLastError();
 }

@@ -129,7 +129,8 @@ __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned 
 // block and the wave's vocabulary rows v0 + 32wv + 8*(reg/4) + 4h + reg%4
 // (increasing with reg). Adds the EOS bias, folds the 16 logits into
 // (max, sum exp) and a sorted best-KB key list, then combines lanes l and
-// l+32 (same row), which end with identical results.
+// l+32 (same row), which end with identical results. KB = 4 takes a
+// cheaper network than a full sort.
 template <int KB>
 __device__ __forceinline__ void block_lists(const f16v &z, int v0, int wv, int h, int V, float bias, float &m_out,
                                             float &s_out, TopK<KB> &tk) {
@@ -152,10 +153,17 @@ __device__ __forceinline__ void block_lists(const f16v &z, int v0, int wv, int h
   cand_key keys[16];
 #pragma unroll
   for (int reg = 0; reg < 16; ++reg) keys[reg] = make_key(vals[reg], v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3));
-  bitonic_sort_desc<16>(keys);
+  TopK<KB> mine;
+  if constexpr (KB == 4) {
+    top4_of_16(keys, mine);
+  } else {
+    bitonic_sort_desc<16>(keys);
+#pragma unroll
+    for (int q = 0; q < KB; ++q) mine.k[q] = keys[q];
+  }
   TopK<KB> lo, hi;
 #pragma unroll
-  for (int q = 0; q < KB; ++q) stage64<5>(keys[q], lo.k[q], hi.k[q]);
+  for (int q = 0; q < KB; ++q) stage64<5>(mine.k[q], lo.k[q], hi.k[q]);
   topk_merge(lo, hi);
   tk = lo;
   uint32_t ma, mb, sa, sb;
@@ -478,7 +486,7 @@ template <bool BF16>
 hipError_t launch_proj_t(const DevState &st, hipStream_t s) {
   // Multiple of 8, at most one per compute unit, no more than the tiles of a full step.
   const int G = std::max(8, std::min(st.n_cu / 8 * 8, xcd_grid(st.S * ((st.R_max + TR - 1) / TR))));
-  switch (st.kbucket) {
+  switch (st.tile_keys) {
     case 4: hipLaunchKernelGGL((k_proj<BF16, 4>), dim3(G), dim3(THREADS), 0, s, st); break;
     case 8: hipLaunchKernelGGL((k_proj<BF16, 8>), dim3(G), dim3(THREADS), 0, s, st); break;
     default: hipLaunchKernelGGL((k_proj<BF16, 16>), dim3(G), dim3(THREADS), 0, s, st); break;

@@ -26,6 +26,7 @@ struct DevCtrl {
   int32_t pad0;
   int64_t timesteps, expansions, noops, refills, admitted, hyps, finished;
   int64_t positions;       // output positions t of the expanded rows, summed
+  int64_t tile_recomputes; // (row, tile) pairs recomputed by the row merge
   int64_t rows_hist[64];   // timesteps by rows expanded, bucket = R / hist_width
 };
 
@@ -97,6 +98,7 @@ struct DevState {
   int32_t attn;        // 1: projection input = h + layer-mean attention read-out
   int32_t anc_stride;  // bytes per slot of anc: max_len_cap rounded up to 4
   int32_t kbucket;     // top-k list length used by the kernels: 4, 8 or 16 (>= k)
+  int32_t tile_keys;   // keys per (row, vocabulary tile) partial record: 4 or kbucket
   int32_t hist_width;  // rows per bucket of DevCtrl::rows_hist
   int32_t n_cu;        // compute units of the device (persistent launches)
   int32_t select_all;  // 1: expand every live beam (Var-Str-FIFO), 0: minimal l_t only

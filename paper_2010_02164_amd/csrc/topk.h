@@ -107,6 +107,40 @@ __device__ __forceinline__ void topk_load(TopK<K> &t, const float *p) {
 // padded to a multiple of 4 so that records are 16-byte aligned.
 __host__ __device__ constexpr int part_width(int kb) { return (2 + 2 * kb + 3) & ~3; }
 
+// Short per-(row, vocabulary tile) key list of the projection, used when the
+// vocabulary has many tiles: a tile holding more of a row's best k than
+// this is found by the row merge (its last kept key still ranks among the
+// best k) and recomputed there; with few tiles that is common, and the list
+// holds the full k-bucket instead.
+constexpr int TILE_KEYS_SHORT = 4;
+
+// The best 4 of 16 keys, sorted: four sorted groups of 4 (bitonic), merged
+// pairwise keeping the best 4.
+__device__ __forceinline__ void top4_of_16(cand_key *a, TopK<4> &out) {
+  TopK<4> g[4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) g[x].k[j] = a[4 * x + j];
+    bitonic_sort_desc<4>(g[x].k);
+  }
+  topk_merge(g[0], g[1]);
+  topk_merge(g[2], g[3]);
+  topk_merge(g[0], g[2]);
+  out = g[0];
+}
+
+// Insert one key into a sorted list (the smallest key falls off).
+template <int K>
+__device__ __forceinline__ void topk_insert(TopK<K> &t, cand_key x) {
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const cand_key hi = t.k[j] > x ? t.k[j] : x;
+    x = t.k[j] > x ? x : t.k[j];
+    t.k[j] = hi;
+  }
+}
+
 // (m, s) represents log(s) + m: a running max and a sum of exp(z - m).
 __device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2) {
   const float M = fmaxf(m, m2);

@@ -129,3 +129,26 @@ def test_cfg3_full_size_sampled(gpu):
     rep = compare(hy, mm, [[(h.tokens, h.score, h.status) for h in g[i]] for i in sample], inputs=sample)
     print(f"[parity] cfg3 full, sampled: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures
+
+
+def _clustered(cfg, seed=5):
+    # Eight near-copies of one W_out row with a large norm inside the first
+    # 128-token tile: most rows then have several of their best k there, and
+    # the projection's 4-key tile list must be completed by the row merge.
+    from oracle.decoder import bf16_round
+    wl = make_workload(cfg)
+    rng = np.random.default_rng(seed)
+    base = wl.W_out[1] * 4.0
+    for v in range(1, 9):
+        row = base + rng.standard_normal(wl.cfg.d).astype(np.float32) * 0.02
+        wl.W_out[v] = bf16_round(row).astype(np.float32) if wl.is_bf16 else row
+    return wl
+
+
+@pytest.mark.parametrize("cfg", [scaled(1, N=40, k=8, M=8, V=8192), scaled(4, N=24, n=8, V=8192, d=256, k=6)],
+                         ids=["f32_k8", "bf16_k6"])
+def test_tile_list_completion(gpu, cfg):
+    # 64 tiles of 128 tokens: the projection keeps 4 keys per tile.
+    wl = _clustered(cfg)
+    rep, g, st, o = check_parity(wl, "var_stream")
+    assert st["tile_recomputes"] > 0
