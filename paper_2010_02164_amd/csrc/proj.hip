@@ -397,22 +397,16 @@ template <bool BF16, int KB>
 __device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, int vt, int rt, int R, int bt) {
   const int r0 = rt * bt * 32;
   const int nbt = min(bt, (R - r0 + 31) >> 5);   // blocks holding valid rows
-  if constexpr (BF16) {
+  if (nbt <= NB)
     proj_tile_ksplit<BF16, KB>(st, sm, vt, r0, R, nbt);
-  } else {
-    if (nbt <= NB)
-      proj_tile_ksplit<BF16, KB>(st, sm, vt, r0, R, nbt);
-    else
-      proj_tile_big<BF16, KB>(st, sm, vt, r0, R, nbt);
-  }
+  else
+    proj_tile_big<BF16, KB>(st, sm, vt, r0, R, nbt);
 }
 
 // Blocks per row tile for a step of R rows: the count (1..8) that minimizes
 // rounds x tile cost, where a round is one tile per workgroup and a tile
 // costs its MFMA blocks (a big tile computes an even count) plus a fixed
 // part worth 0.7 block (prologue, epilogue). Ties go to the larger tile.
-// The bf16 path keeps 4-block tiles: its MFMA blocks are cheap next to the
-// per-block epilogue, so fewer rounds of larger tiles do not pay there.
 __device__ __forceinline__ int row_tile_blocks(int R, int S, int G) {
   const int B = (R + 31) >> 5;
   int best_bt = NB;
@@ -444,7 +438,7 @@ template <bool BF16, int KB>
 __global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
   const int R = st.ctrl->R;
   if (R <= 0) return;
-  const int bt = BF16 ? NB : row_tile_blocks(R, st.S, (int)gridDim.x);
+  const int bt = row_tile_blocks(R, st.S, (int)gridDim.x);
   const int nra = (R + 32 * bt - 1) / (32 * bt);
   const int T = st.S * nra;
   const int x = blockIdx.x & 7, gx = gridDim.x >> 3, j = blockIdx.x >> 3;
