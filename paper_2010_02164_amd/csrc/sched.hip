@@ -40,55 +40,11 @@ __device__ int block_excl_scan(int v, int *sm, int *total) {
   return res;
 }
 
-__device__ int block_min(int v, int *sm) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
-  if (lane == 0) sm[w] = v;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int m = sm[0];
-    for (int i = 1; i < nw; ++i) m = min(m, sm[i]);
-    sm[nw] = m;
-  }
-  __syncthreads();
-  int r = sm[nw];
-  __syncthreads();
-  return r;
-}
-
 // Each thread owns a contiguous range of at most SCHED_MAXB beams (so rows
-// come out in beam order) and keeps their records in registers; every
-// decision needs one block-wide scan or reduction.
+// come out in beam order) and keeps their records in registers.
 constexpr int SCHED_MAXB = 4;
 constexpr int SCHED_MAXP = SCHED_THREADS * SCHED_MAXB;   // beam records
 constexpr int SCHED_MAXL = 4096;                         // l_t bins (max_len_cap)
-
-__device__ long long block_excl_scan64(long long v, long long *sm, long long *total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  long long x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const long long y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) sm[w] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    long long acc = 0;
-    for (int i = 0; i < nw; ++i) {
-      const long long t = sm[i];
-      sm[i] = acc;
-      acc += t;
-    }
-    sm[nw] = acc;
-  }
-  __syncthreads();
-  const long long res = sm[w] + x - v;
-  *total = sm[nw];
-  __syncthreads();
-  return res;
-}
 
 // Capacity-constrained selection works on the live beams in admission
 // order: b_order lists their records (the previous step's live beams, then
@@ -109,21 +65,22 @@ struct CapSmem {
 // with the thread's records (inp, stp) and its kept positions of the old
 // order list (orec); nlive = live beams after admission. Leaves cs.sel[b]
 // set for the selected records and writes the new order list to b_order.
+template <int PER>
 __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *inp, const int *stp,
                            const int *orec, int b0, int nb, int nlive) {
   const int k = st.k;
   // Kept positions are compacted in order ahead of the admitted beams.
   int kept_l = 0;
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) kept_l += u < nb && orec[u] >= 0;
+  for (int u = 0; u < PER; ++u) kept_l += u < nb && orec[u] >= 0;
   int kept_tot;
   int pos = block_excl_scan(kept_l, sm, &kept_tot);
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u)
+  for (int u = 0; u < PER; ++u)
     if (u < nb && orec[u] >= 0) cs.ord[pos++] = orec[u];
   // Per record: l_t and active width (a fresh beam has one candidate).
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) {
+  for (int u = 0; u < PER; ++u) {
     if (u < nb) {
       const int b = b0 + u;
       cs.sel[b] = 0;
@@ -139,9 +96,9 @@ __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *
   }
   __syncthreads();
   // New order list to memory; active width per l_t.
-  int oinfo[SCHED_MAXB], orid[SCHED_MAXB];
+  int oinfo[PER], orid[PER];
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) {
+  for (int u = 0; u < PER; ++u) {
     orid[u] = -1;
     oinfo[u] = 0;
     if (u < nb && b0 + u < nlive) {
@@ -174,12 +131,12 @@ __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *
   // At l*, beams are taken in admission order while they fit.
   int lv = 0;
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u)
+  for (int u = 0; u < PER; ++u)
     if (orid[u] >= 0 && (oinfo[u] >> 8) == lstar) lv += oinfo[u] & 0xff;
   int ltot;
   int e = block_excl_scan(lv, sm, &ltot);
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) {
+  for (int u = 0; u < PER; ++u) {
     if (orid[u] >= 0) {
       const int s = oinfo[u] >> 8, w = oinfo[u] & 0xff;
       bool take = s < lstar;
@@ -193,26 +150,34 @@ __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *
   __syncthreads();
 }
 
+// The scheduler proper. PER = beams per thread (a contiguous range, so rows
+// come out in beam order). Every beam and slot field it needs is loaded at
+// the start in one batch; the step then takes two barrier phases (plus the
+// capacity selection's): live/free counts with the minimal l_t, then the
+// row offsets with the step's totals.
+template <int PER>
 __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
-  __shared__ long long sm64[SCHED_THREADS / 64 + 1];
-  __shared__ int sm[SCHED_THREADS / 64 + 1];
+  constexpr int NW = SCHED_THREADS / 64;
+  __shared__ long long ph1[NW + 1];
+  __shared__ int ph1_min[NW + 1];
+  __shared__ int ph2[4][NW + 1];
+  __shared__ int sm[NW + 1];
   __shared__ CapSmem cs;
   DevCtrl *c = st.ctrl;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = st.n, k = st.k;
   const int nq = c->n_queued, cursor = c->cursor;
-  const int per = (n + SCHED_THREADS - 1) / SCHED_THREADS;   // <= SCHED_MAXB
-  const int b0 = min(n, tid * per), nb = min(n, b0 + per) - b0;
+  const int b0 = min(n, tid * PER), nb = min(n, b0 + PER) - b0;
   const bool cap = st.cap != 0;
 
   // Capacity mode: this thread's positions b0 .. b0+nb-1 of the order list
   // (which holds the live + admitted count of the previous step), read
   // before any record changes below; a beam that finished since is dropped.
-  int orec[SCHED_MAXB];
+  int orec[PER];
   if (cap) {
     const int nord = c->live;
 #pragma unroll
-    for (int u = 0; u < SCHED_MAXB; ++u) {
+    for (int u = 0; u < PER; ++u) {
       orec[u] = -1;
       if (u < nb && b0 + u < nord) {
         const int r = st.b_order[b0 + u];
@@ -226,21 +191,73 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     }
   }
 
-  int inp[SCHED_MAXB], stp[SCHED_MAXB];
-  int live_l = 0;
+  // Beam records, slot states (active / terminated masks) and, with one beam
+  // per thread, the slots' last tokens.
+  int inp[PER], stp[PER];
+  uint32_t amask[PER], tmask[PER];
+  int tok[PER == 1 ? KMAX_SUPPORTED : 1];
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) {
+  for (int u = 0; u < PER; ++u) {
     inp[u] = -1;
     stp[u] = 0;
+    amask[u] = 0u;
+    tmask[u] = 0u;
     if (u < nb) {
       inp[u] = st.b_input[b0 + u];
       stp[u] = st.b_steps[b0 + u];
-      live_l += inp[u] >= 0;
+      for (int j = 0; j < k; ++j) {
+        const int status = st.s_status[(b0 + u) * k + j];
+        amask[u] |= (uint32_t)(status == SLOT_ACTIVE) << j;
+        tmask[u] |= (uint32_t)(status == SLOT_EOS || status == SLOT_MAXLEN) << j;
+      }
     }
   }
-  // One scan: live beams (low 32 bits) and free beams (high 32 bits).
-  long long tot;
-  const long long pre = block_excl_scan64(((long long)(nb - live_l) << 32) | live_l, sm64, &tot);
+  if constexpr (PER == 1) {
+    if (nb > 0)
+      for (int j = 0; j < k; ++j) tok[j] = st.s_tok[b0 * k + j];
+  }
+
+  // Phase 1: live (low word) and free (high word) records, exclusive over
+  // threads, and the minimal l_t of the live beams.
+  int live_l = 0, mn_l = INT_MAX;
+#pragma unroll
+  for (int u = 0; u < PER; ++u)
+    if (u < nb && inp[u] >= 0) {
+      ++live_l;
+      mn_l = min(mn_l, stp[u]);
+    }
+  long long pre, tot;
+  int mn0;
+  {
+    const long long v = ((long long)(nb - live_l) << 32) | live_l;
+    long long x = v;
+    int mm = mn_l;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const long long y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+      mm = min(mm, __shfl_xor(mm, o, 64));
+    }
+    if (lane == 63) ph1[w] = x;
+    if (lane == 0) ph1_min[w] = mm;
+    __syncthreads();
+    if (tid == 0) {
+      long long acc = 0;
+      int m = INT_MAX;
+      for (int i = 0; i < NW; ++i) {
+        const long long t = ph1[i];
+        ph1[i] = acc;
+        acc += t;
+        m = min(m, ph1_min[i]);
+      }
+      ph1[NW] = acc;
+      ph1_min[NW] = m;
+    }
+    __syncthreads();
+    pre = ph1[w] + x - v;
+    tot = ph1[NW];
+    mn0 = ph1_min[NW];
+  }
   const int live = (int)(tot & 0xffffffff);
 
   // Refill (Alg. 1): if inputs remain and |B| <= eps*n, admit
@@ -251,12 +268,15 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
   if (admit > 0) {
     int rank = (int)(pre >> 32);
 #pragma unroll
-    for (int u = 0; u < SCHED_MAXB; ++u) {
+    for (int u = 0; u < PER; ++u) {
       if (u < nb && inp[u] < 0) {
         if (rank < admit) {
           const int b = b0 + u;
           inp[u] = cursor + rank;
           stp[u] = 0;
+          amask[u] = 1u;
+          tmask[u] = 0u;
+          if constexpr (PER == 1) tok[0] = 0;
           st.b_input[b] = inp[u];
           st.b_steps[b] = 0;
           st.b_par[b] = 0;
@@ -274,53 +294,85 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     }
   }
 
-  // Selection: the live beams with the fewest steps taken, or every live
-  // beam (Var-Str-FIFO: the capacity n, from the beam with the most steps
-  // down, covers all of them), or the capacity-constrained prefix.
-  int mn_l = INT_MAX;
-#pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u)
-    if (u < nb && inp[u] >= 0) mn_l = min(mn_l, stp[u]);
-  const int mn = block_min(mn_l, sm);
-  if (cap) cap_select(st, cs, sm, inp, stp, orec, b0, nb, live + admit);
+  // Selection: the live beams with the fewest steps taken (an admitted beam
+  // has taken none), or every live beam (Var-Str-FIFO: the capacity n, from
+  // the beam with the most steps down, covers all of them), or the
+  // capacity-constrained prefix.
+  const int mn = admit > 0 ? 0 : mn0;
+  if (cap) cap_select<PER>(st, cs, sm, inp, stp, orec, b0, nb, live + admit);
 
-  // Active and terminated candidates of the selected beams (slot order);
-  // each beam's active slots are kept as a bit mask.
+  bool sel[PER];
   int act_l = 0, term_l = 0, sel_l = 0, pos_l = 0;
-  uint32_t amask[SCHED_MAXB];
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) {
-    amask[u] = 0u;
-    const bool sel = u < nb && inp[u] >= 0 && (cap ? cs.sel[b0 + u] != 0 : (st.select_all || stp[u] == mn));
-    sel_l += sel;
-    if (sel) {
-      for (int j = 0; j < k; ++j) {
-        const int status = st.s_status[(b0 + u) * k + j];
-        amask[u] |= (uint32_t)(status == SLOT_ACTIVE) << j;
-        term_l += status == SLOT_EOS || status == SLOT_MAXLEN;
-      }
+  for (int u = 0; u < PER; ++u) {
+    sel[u] = u < nb && inp[u] >= 0 && (cap ? cs.sel[b0 + u] != 0 : (st.select_all || stp[u] == mn));
+    if (sel[u]) {
+      ++sel_l;
       act_l += __popc(amask[u]);
+      term_l += __popc(tmask[u]);
       pos_l += __popc(amask[u]) * (stp[u] + 1);
+    } else {
+      amask[u] = 0u;
     }
   }
-  long long tot2;
-  const long long pre2 = block_excl_scan64(((long long)term_l << 32) | act_l, sm64, &tot2);
-  const int R = (int)(tot2 & 0xffffffff);
-  const int noops = (int)(tot2 >> 32);
-  int row = (int)(pre2 & 0xffffffff);
+  // Phase 2: row offsets (exclusive scan of active candidates) and the
+  // step's totals of rows, no-ops, selected beams and output positions.
+  int row, R, noops, nsel, npos;
+  {
+    int x = act_l, a = term_l, b = sel_l, q = pos_l;
 #pragma unroll
-  for (int u = 0; u < SCHED_MAXB; ++u) {
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+      a += __shfl_xor(a, o, 64);
+      b += __shfl_xor(b, o, 64);
+      q += __shfl_xor(q, o, 64);
+    }
+    if (lane == 63) ph2[0][w] = x;
+    if (lane == 0) {
+      ph2[1][w] = a;
+      ph2[2][w] = b;
+      ph2[3][w] = q;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int acc = 0, ta = 0, tb = 0, tq = 0;
+      for (int i = 0; i < NW; ++i) {
+        const int t = ph2[0][i];
+        ph2[0][i] = acc;
+        acc += t;
+        ta += ph2[1][i];
+        tb += ph2[2][i];
+        tq += ph2[3][i];
+      }
+      ph2[0][NW] = acc;
+      ph2[1][NW] = ta;
+      ph2[2][NW] = tb;
+      ph2[3][NW] = tq;
+    }
+    __syncthreads();
+    row = ph2[0][w] + x - act_l;
+    R = ph2[0][NW];
+    noops = ph2[1][NW];
+    nsel = ph2[2][NW];
+    npos = ph2[3][NW];
+  }
+
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
     if (u < nb) {
       const int b = b0 + u;
-      const bool sel = inp[u] >= 0 && (cap ? cs.sel[b] != 0 : (st.select_all || stp[u] == mn));
-      st.b_sel[b] = sel;
-      const int lx = sel ? st.q_Lx[inp[u]] : 0;
+      st.b_sel[b] = sel[u];
+      const int lx = sel[u] ? st.q_Lx[inp[u]] : 0;
       for (int j = 0; j < k; ++j) {
         const int s = b * k + j;
         if ((amask[u] >> j) & 1u) {
+          int y;
+          if constexpr (PER == 1) y = tok[j];
+          else y = st.s_tok[s];
           st.r_slot[row] = s;
           st.r_hsrc[row] = stp[u] == 0 ? -1 - inp[u] : s;   // a fresh beam reads its encoding h0
-          st.r_y[row] = st.s_tok[s];
+          st.r_y[row] = y;
           st.r_t[row] = stp[u] + 1;
           st.r_Lx[row] = lx;
           st.s_row[s] = row;
@@ -331,9 +383,6 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
       }
     }
   }
-  int nsel, npos;
-  block_excl_scan(sel_l, sm, &nsel);
-  block_excl_scan(pos_l, sm, &npos);
 
   if (tid == 0) {
     c->cursor = cursor + admit;
@@ -381,7 +430,10 @@ __global__ void k_init(DevState st) {
 }  // namespace
 
 hipError_t launch_sched(const DevState &st, hipStream_t s) {
-  hipLaunchKernelGGL(k_sched, dim3(1), dim3(SCHED_THREADS), 0, s, st);
+  const int per = (st.n + SCHED_THREADS - 1) / SCHED_THREADS;
+  if (per <= 1) hipLaunchKernelGGL(k_sched<1>, dim3(1), dim3(SCHED_THREADS), 0, s, st);
+  else if (per == 2) hipLaunchKernelGGL(k_sched<2>, dim3(1), dim3(SCHED_THREADS), 0, s, st);
+  else hipLaunchKernelGGL(k_sched<4>, dim3(1), dim3(SCHED_THREADS), 0, s, st);
   return hipGetLastError();
 }
 
