@@ -39,7 +39,9 @@ union ProjSmem {
   unsigned char B[2][2][TR][LS];          // [buffer][wave group][row][byte]
   float red[2][4][2][16][64];             // [sending half][slice][block][reg][lane]
   float xch[4][TR][part_width(KB)];       // [slice][row][max, sumexp, keys]
-  float xr[2][2][4][32][part_width(KB)];  // [buffer][group][slice][row][...], one block at a time
+  // [buffer][group][slice][row][...]: with 4-key lists one buffer per owned
+  // block, else two used in turn
+  float xr[KB == 4 ? NB : 2][2][4][32][part_width(KB)];
 };
 
 // K loop of one wave over its half: acc[b] (b < NBV) += W_out fragment x
@@ -355,14 +357,13 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
       proj_mainloop<BF16, 4, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
   }
 
-  // Epilogue, one owned block at a time: lane lists, then wave i of the
-  // group merges block i's four vocabulary slices (double-buffered LDS).
+  if constexpr (KB == 4) {
+    // Epilogue: the lane lists of every owned block, then wave i of each
+    // group merges block i's four vocabulary slices, all blocks at once.
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    if (i < nbh) {
+    for (int i = 0; i < NB; ++i) {
       const int blk = gb0 + i;
-      const int buf = i & 1;
-      if (blk < nbt) {
+      if (i < nbh && blk < nbt) {
         f16v z;
 #pragma unroll
         for (int reg = 0; reg < 16; ++reg) z[reg] = acc0[i][reg] + acc1[i][reg];
@@ -372,19 +373,54 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
         TopK<KB> tk;
         block_lists<KB>(z, v0, wv, h, V, bias, m, s, tk);
         if (lane < 32) {
-          float *p = sm.xr[buf][g][wv][l32];
+          float *p = sm.xr[i][g][wv][l32];
           p[0] = m;
           p[1] = s;
           topk_store(p + 2, tk);
         }
       }
-      __syncthreads();
-      if (blk < nbt && wv == i && lane < 32) {
-        const int j = r0 + 32 * blk + l32;
-        if (j < R) {
-          const float *sl[4] = {sm.xr[buf][g][0][l32], sm.xr[buf][g][1][l32], sm.xr[buf][g][2][l32],
-                                sm.xr[buf][g][3][l32]};
-          write_record<KB>(st, j, vt, sl);
+    }
+    __syncthreads();
+    const int blk = gb0 + wv;
+    if (wv < nbh && blk < nbt && lane < 32) {
+      const int j = r0 + 32 * blk + l32;
+      if (j < R) {
+        const float *sl[4] = {sm.xr[wv][g][0][l32], sm.xr[wv][g][1][l32], sm.xr[wv][g][2][l32], sm.xr[wv][g][3][l32]};
+        write_record<KB>(st, j, vt, sl);
+      }
+    }
+  } else {
+    // Epilogue, one owned block at a time: lane lists, then wave i of the
+    // group merges block i's four vocabulary slices (double-buffered LDS).
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if (i < nbh) {
+        const int blk = gb0 + i;
+        const int buf = i & 1;
+        if (blk < nbt) {
+          f16v z;
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) z[reg] = acc0[i][reg] + acc1[i][reg];
+          const int j = r0 + 32 * blk + l32;
+          const float bias = (v0 == 0 && j < R) ? st.beta * (float)(st.r_t[j] - st.r_Lx[j]) : 0.0f;
+          float m, s;
+          TopK<KB> tk;
+          block_lists<KB>(z, v0, wv, h, V, bias, m, s, tk);
+          if (lane < 32) {
+            float *p = sm.xr[buf][g][wv][l32];
+            p[0] = m;
+            p[1] = s;
+            topk_store(p + 2, tk);
+          }
+        }
+        __syncthreads();
+        if (blk < nbt && wv == i && lane < 32) {
+          const int j = r0 + 32 * blk + l32;
+          if (j < R) {
+            const float *sl[4] = {sm.xr[buf][g][0][l32], sm.xr[buf][g][1][l32], sm.xr[buf][g][2][l32],
+                                  sm.xr[buf][g][3][l32]};
+            write_record<KB>(st, j, vt, sl);
+          }
         }
       }
     }
