@@ -42,6 +42,7 @@ union ProjSmem {
   // [buffer][group][slice][row][...]: with 4-key lists one buffer per owned
   // block, else two used in turn
   float xr[KB == 4 ? NB : 2][2][4][32][part_width(KB)];
+  float xw[KB == 4 ? 2 : 1][4][TR][part_width(KB)];   // wide tile: [128-row vocabulary tile][slice][row][...]
 };
 
 // K loop of one wave over its half: acc[b] (b < NBV) += W_out fragment x
@@ -49,17 +50,22 @@ union ProjSmem {
 // (+ lane * 16 + q * 1 KB), the half's state tile at bbase + c * 128 bytes
 // (+ boff[u]). Loads of a chunk are issued together, D chunks ahead of use,
 // at indices clamped to the last chunk so that no load sits in a branch.
-template <bool BF16, int NBV, int D>
+// With NA = 2 the wave covers two adjacent 32-row vocabulary slices
+// (fragments at abase and abase + WCH) and acc[x * NBV + bb] is slice x,
+// block bb; each state fragment read from LDS then feeds two MFMAs.
+template <bool BF16, int NBV, int D, int NA = 1>
 __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned char (*Bt1)[LS],
                                               const unsigned char *abase, uint32_t alane,
                                               const unsigned char *bbase, const uint32_t *boff, int srow,
                                               int scol, int nh, int l32, int h, f16v *acc) {
-  u4 a[D][4];
+  u4 a[D][NA * 4];
   u4 b[D][NBV];
   auto loadA = [&](int c, u4 *dst) {
     const unsigned char *p = abase + (uint32_t)c * (uint32_t)(4 * WCH);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) dst[q] = *reinterpret_cast<const u4 *>(p + alane + q * FRAG);
+    for (int x = 0; x < NA; ++x)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) dst[4 * x + q] = *reinterpret_cast<const u4 *>(p + x * WCH + alane + q * FRAG);
   };
   auto loadB = [&](int c, u4 *dst) {
     const unsigned char *p = bbase + (uint32_t)c * CH;
@@ -80,14 +86,18 @@ __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned 
       for (int bb = 0; bb < NBV; ++bb) braw[bb] = *reinterpret_cast<const u4 *>(&T[32 * bb + l32][64 * h + 16 * q]);
 #pragma unroll
       for (int bb = 0; bb < NBV; ++bb) {
-        if constexpr (BF16) {
-          acc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, af[q]),
-                                                            __builtin_bit_cast(bf8, braw[bb]), acc[bb], 0, 0, 0);
-        } else {
-          const f4 av = __builtin_bit_cast(f4, af[q]);
-          const f4 bv = __builtin_bit_cast(f4, braw[bb]);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc[bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], acc[bb], 0, 0, 0);
+        for (int x = 0; x < NA; ++x) {
+          f16v &c = acc[x * NBV + bb];
+          if constexpr (BF16) {
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, af[4 * x + q]),
+                                                        __builtin_bit_cast(bf8, braw[bb]), c, 0, 0, 0);
+          } else {
+            const f4 av = __builtin_bit_cast(f4, af[4 * x + q]);
+            const f4 bv = __builtin_bit_cast(f4, braw[bb]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], c, 0, 0, 0);
+          }
         }
       }
     }
@@ -427,6 +437,91 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
   }
 }
 
+// Wide tile (bf16, 4-key lists): 256 vocabulary rows x 128 batch rows. Wave
+// w sums K half w/4 over vocabulary rows 64*(w%4) .. +63 (two 32-row slices)
+// of the 256 and all four blocks, so each state fragment read from LDS
+// feeds two MFMAs (the LDS reads per MFMA halve next to a 32-row wave). The
+// K halves and each half's MFMA sequence are those of the other tiles, so
+// the sums are the same. vw: 256-row vocabulary tile; its second 128-row
+// half may lie past the vocabulary (odd tile count): those waves compute a
+// copy of the last tile and write nothing.
+template <int KB>
+__device__ __forceinline__ void proj_tile_wide(const DevState &st, ProjSmem<KB> &sm, int vw, int r0, int R) {
+  const int d = st.d, V = st.V;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = w >> 2, vq = w & 3;               // K half, vocabulary quarter
+  const int l32 = lane & 31, h = lane >> 5;
+  const int rowbytes = d * 2;
+  const int nk = rowbytes / CH, nh = nk >> 1, kbeg = g * nh;
+  const int t2 = vq >> 1;                          // which 128-row half of the 256
+  const int vt = min(2 * vw + t2, st.S - 1);       // 128-row tile of this wave's rows
+  const int s0 = 2 * (vq & 1);                     // its first slice in that tile
+  const int v0 = vt * TV;
+  const unsigned char *abase = st.wout_t + ((size_t)(vt * nk + kbeg) * 4 + s0) * WCH;
+  const int tg = tid & 255;
+  const int srow = tg >> 3, scol = (tg & 7) * 16;
+  uint32_t boff[NB];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) boff[u] = (uint32_t)min(r0 + srow + 32 * u, R - 1) * (uint32_t)rowbytes + scol;
+  const unsigned char *bbase = static_cast<const unsigned char *>(st.proj_in) + (size_t)kbeg * CH;
+  f16v acc[2 * NB];
+#pragma unroll
+  for (int b = 0; b < 2 * NB; ++b) acc[b] = f16v{};
+  proj_mainloop<true, NB, 2, 2>(sm.B[0][g], sm.B[1][g], abase, (uint32_t)lane * 16u, bbase, boff, srow, scol, nh,
+                                l32, h, acc);
+
+  // Combine the halves, one slice at a time: half g owns blocks 2g, 2g+1,
+  // sends its sums of the other two and adds the received ones once.
+  f16v own[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+#pragma unroll
+    for (int bl = 0; bl < 2; ++bl) {
+      const f16v snd = acc[x * NB + (g ? bl : 2 + bl)];
+      own[x][bl] = acc[x * NB + (g ? 2 + bl : bl)];
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) sm.red[g][vq][bl][reg][lane] = snd[reg];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int bl = 0; bl < 2; ++bl)
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) own[x][bl][reg] += sm.red[1 - g][vq][bl][reg][lane];
+    __syncthreads();
+  }
+
+  // Lane lists of the four owned (slice, block) tiles, then wave w merges
+  // the four slices of 128-row tile w/4, block w%4.
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+#pragma unroll
+    for (int bl = 0; bl < 2; ++bl) {
+      const int blk = 2 * g + bl;
+      const int j = r0 + 32 * blk + l32;
+      const float bias = (v0 == 0 && j < R) ? st.beta * (float)(st.r_t[j] - st.r_Lx[j]) : 0.0f;
+      float m, s;
+      TopK<KB> tk;
+      block_lists<KB>(own[x][bl], v0, s0 + x, h, V, bias, m, s, tk);
+      if (lane < 32) {
+        float *p = sm.xw[t2][s0 + x][32 * blk + l32];
+        p[0] = m;
+        p[1] = s;
+        topk_store(p + 2, tk);
+      }
+    }
+  }
+  __syncthreads();
+  {
+    const int mt = w >> 2, row = 32 * (w & 3) + l32;
+    const int j = r0 + row;
+    if (lane < 32 && j < R && 2 * vw + mt < st.S) {
+      const float *sl[4] = {sm.xw[mt][0][row], sm.xw[mt][1][row], sm.xw[mt][2][row], sm.xw[mt][3][row]};
+      write_record<KB>(st, j, 2 * vw + mt, sl);
+    }
+  }
+}
+
 // Row tile rt covers blocks bt*rt .. bt*rt + bt - 1 (32 rows each) of
 // vocabulary tile vt.
 template <bool BF16, int KB>
@@ -474,9 +569,12 @@ template <bool BF16, int KB>
 __global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
   const int R = st.ctrl->R;
   if (R <= 0) return;
-  const int bt = row_tile_blocks(R, st.S, (int)gridDim.x);
-  const int nra = (R + 32 * bt - 1) / (32 * bt);
-  const int T = st.S * nra;
+  // bf16 steps whose 256-wide tiles fill at least one round use them.
+  const int S2 = (st.S + 1) >> 1, nrw = (R + TR - 1) / TR;
+  const bool wide = BF16 && KB == 4 && S2 * nrw >= (int)gridDim.x;
+  const int bt = wide ? NB : row_tile_blocks(R, st.S, (int)gridDim.x);
+  const int nra = wide ? nrw : (R + 32 * bt - 1) / (32 * bt);
+  const int T = (wide ? S2 : st.S) * nra;
   const int x = blockIdx.x & 7, gx = gridDim.x >> 3, j = blockIdx.x >> 3;
   const int lo = (int)((long long)T * x / 8), nt = (int)((long long)T * (x + 1) / 8) - lo;
   __shared__ ProjSmem<KB> sm;
@@ -485,6 +583,13 @@ __global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
     if (idx >= nt) continue;
     const int tile = lo + idx;
     const int vt = tile / nra, rt = tile - vt * nra;
+    if constexpr (BF16 && KB == 4) {
+      if (wide) {
+        proj_tile_wide<KB>(st, sm, vt, rt * TR, R);
+        __syncthreads();   // LDS is reused by the next tile
+        continue;
+      }
+    }
     proj_tile<BF16, KB>(st, sm, vt, rt, R, bt);
     __syncthreads();   // LDS is reused by the next tile
   }

@@ -7,7 +7,7 @@ import pytest
 from oracle.decoder import ElmanDecoder
 from synthgen import make_workload, scaled
 from synthgen.gen import bf16_bits_to_f32, f32_to_bf16_bits
-from tests.gpu_util import check_parity
+from tests.gpu_util import check_parity, gpu_decode
 
 pytestmark = pytest.mark.gpu
 
@@ -82,3 +82,23 @@ def test_cfg5_kv_rows(gpu, sched):
     # fp32-accumulated bf16 products vs the fp64 value: at most one bf16 step
     assert d.max() <= 1
     assert np.mean(d == 0) > 0.99
+
+
+def test_bf16_schedulers_agree_bitwise_across_tile_shapes(gpu):
+    # |V| = 32000 with steps of up to 640 rows: large steps use 256-wide
+    # vocabulary tiles, small ones 128-wide tiles of 1 to 8 blocks; a row's
+    # sums must not depend on which.
+    wl = make_workload(scaled(4, N=96, n=64, V=32000, d=256))
+    a, sa, da = gpu_decode(wl, "var_batch")
+    counts, width = da.rows_histogram()
+    assert sum(c for i, c in enumerate(counts) if i * width >= 384) > 0
+    for sched, kw in (("var_stream", {}), ("var_fifo", dict(n=24)), ("var_cap", dict(n=40, pool=80))):
+        b, sb, _ = gpu_decode(wl, sched, **kw)
+        assert sb["expansions"] == sa["expansions"]
+        for ya, yb in zip(a, b):
+            assert [(h.tokens, h.score, h.status) for h in ya] == [(h.tokens, h.score, h.status) for h in yb]
+
+
+def test_cfg4_wide_tiles_parity(gpu):
+    wl = make_workload(scaled(4, N=96, n=64, V=32000, d=256))
+    check_parity(wl, "var_stream")

@@ -70,9 +70,12 @@ def test_expand_f32(gpu, cfg_i, R, over):
     _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse)
 
 
-@pytest.mark.parametrize("over", [dict(V=8000, n=32), dict(V=4160, d=256, n=16, k=16)])
+@pytest.mark.parametrize("over", [dict(V=8000, n=32), dict(V=4160, d=256, n=16, k=16),
+                                  dict(V=32000, n=64), dict(V=32128, d=256, n=64)])
 def test_expand_bf16(gpu, over):
+    # The last two use 256-wide vocabulary tiles (640 rows fill a round of
+    # them); 32128 tokens leave the last 256-wide tile half empty.
     wl = make_workload(scaled(4, N=4, **over))
-    _, _, _, _, h_gpu, lse, lp, tok, h_ref, lp_ref = _expand_case(wl, 200, 12)
+    _, _, _, _, h_gpu, lse, lp, tok, h_ref, lp_ref = _expand_case(wl, 640 if over["V"] >= 32000 else 200, 12)
     print(f"[expand] bf16 {over}", flush=True)
     _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse)
