@@ -147,11 +147,16 @@ template <int KB>
 __device__ __forceinline__ void block_lists(const f16v &z, int v0, int wv, int h, int V, float bias, float &m_out,
                                             float &s_out, TopK<KB> &tk) {
   float vals[16];
+  if (v0 != 0 && v0 + TV <= V) {   // interior tile: no EOS bias, no rows past V
 #pragma unroll
-  for (int reg = 0; reg < 16; ++reg) {
-    const int v = v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3);
-    const float zz = v == 0 ? z[reg] + bias : z[reg];
-    vals[reg] = v < V ? zz : -INFINITY;
+    for (int reg = 0; reg < 16; ++reg) vals[reg] = z[reg];
+  } else {
+#pragma unroll
+    for (int reg = 0; reg < 16; ++reg) {
+      const int v = v0 + 32 * wv + 8 * (reg >> 2) + 4 * h + (reg & 3);
+      const float zz = v == 0 ? z[reg] + bias : z[reg];
+      vals[reg] = v < V ? zz : -INFINITY;
+    }
   }
   float m = -INFINITY;
 #pragma unroll

@@ -17,9 +17,10 @@ namespace sb {
 typedef unsigned long long cand_key;
 
 __device__ __forceinline__ cand_key make_key(float v, int idx) {
-  uint32_t u = __float_as_uint(v);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((cand_key)u << 32) | (uint32_t)(~idx);
+  // Negative values: all bits flipped; others: the sign bit set.
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t o = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+  return ((cand_key)o << 32) | (uint32_t)(~idx);
 }
 __device__ __forceinline__ float key_val(cand_key k) {
   uint32_t u = (uint32_t)(k >> 32);
@@ -114,15 +115,20 @@ __host__ __device__ constexpr int part_width(int kb) { return (2 + 2 * kb + 3) &
 // holds the full k-bucket instead.
 constexpr int TILE_KEYS_SHORT = 4;
 
-// The best 4 of 16 keys, sorted: four sorted groups of 4 (bitonic), merged
-// pairwise keeping the best 4.
+// The best 4 of 16 keys, sorted: four groups of 4 sorted by the 5-exchange
+// network, merged pairwise keeping the best 4.
 __device__ __forceinline__ void top4_of_16(cand_key *a, TopK<4> &out) {
   TopK<4> g[4];
 #pragma unroll
   for (int x = 0; x < 4; ++x) {
+    cand_key *k = g[x].k;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) g[x].k[j] = a[4 * x + j];
-    bitonic_sort_desc<4>(g[x].k);
+    for (int j = 0; j < 4; ++j) k[j] = a[4 * x + j];
+    cex(k[0], k[1], true);
+    cex(k[2], k[3], true);
+    cex(k[0], k[2], true);
+    cex(k[1], k[3], true);
+    cex(k[1], k[2], true);
   }
   topk_merge(g[0], g[1]);
   topk_merge(g[2], g[3]);
