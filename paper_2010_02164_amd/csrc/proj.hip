@@ -2,20 +2,28 @@
 // fused with the EOS bias, an online log-sum-exp and a per-row partial top-k:
 //   z = W_out h,  z[0] += beta (t - L_x)      [R,d] x [V,d]^T
 // The R x |V| logits never reach memory: each workgroup writes, per row and
-// 128-wide vocabulary tile, (max, sum exp) and its best kb (value, token).
+// 128-wide vocabulary tile, (max, sum exp) and its best keys (value, token).
 //
-// Workgroup: 8 waves on a tile of 128 vocabulary rows x 128 batch rows (4
-// blocks of 32). The K range is split in two fixed halves: waves 0-3 sum the
-// first half, waves 4-7 the second, each wave over its own 32 vocabulary
-// rows; the two partial sums are added once at the end. Every output
-// therefore accumulates in the same order whatever rows share the step, so a
-// row's result does not depend on the batch.
+// Workgroups of 8 waves walk the step's tiles on a persistent grid. Tile
+// kinds (chosen per step on the device from the row count):
+//   - 128 vocabulary rows x 1..4 blocks of 32 batch rows: the K range is
+//     split in two fixed halves, waves 0-3 summing the first, waves 4-7 the
+//     second, each wave over its own 32 vocabulary rows; the two partial
+//     sums are added once at the end;
+//   - 128 vocabulary rows x 5..8 blocks: each wave group takes half of the
+//     blocks and sums the two K halves one after the other into two
+//     accumulator sets, added once at the end;
+//   - bf16 only, 256 vocabulary rows x 4 blocks: K halves as in the first
+//     kind, each wave over 64 vocabulary rows.
+// In all of them an output accumulates its K halves through the same MFMA
+// sequence and adds them once, so a row's result does not depend on the
+// batch or on the tiling.
 //
 // W_out is streamed straight into registers from a copy laid out in MFMA
 // fragment order (one coalesced 1 KB load per wave and fragment), kept D
 // chunks ahead; the states of each half pass through a double-buffered LDS
-// tile shared by its four waves, loaded D chunks ahead as well. Blocks of 32
-// rows past R are neither loaded nor computed.
+// tile shared by the waves of that half, loaded D chunks ahead as well.
+// Blocks of 32 rows past R are neither loaded nor computed.
 #include <algorithm>
 
 #include "mfma_common.h"
