@@ -36,7 +36,8 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA, MI355X
 # Sources of the projection kernel; measured HBM traffic is reported only
 # while they are unchanged since the counters were taken.
 PROJ_SOURCES = ["paper_2010_02164_amd/csrc/proj.hip", "paper_2010_02164_amd/csrc/topk.h",
-                "paper_2010_02164_amd/csrc/mfma_common.h"]
+                "paper_2010_02164_amd/csrc/mfma_common.h", "paper_2010_02164_amd/csrc/wave.h",
+                "paper_2010_02164_amd/csrc/sb_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_proj_traffic.md")
 METRIC = "finalized hyps/sec + expansions/sec (Var-Stream, k=5, |V|=32k), % roofline"
 
@@ -69,10 +70,16 @@ def cpu_baseline(wl, sched, eps, sample, pool=None):
 
 
 def proj_source_sha256():
+    """Hash of the projection kernel's sources with // comments, trailing
+    blanks and empty lines removed (a comment edit keeps the measured
+    figures valid; any code edit invalidates them)."""
     h = hashlib.sha256()
     for rel in PROJ_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            for line in f:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()
 
 
