@@ -33,6 +33,22 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA, MI355X
+HBM_PEAK_BPS = 8.0e12                            # MI355X HBM3E
+
+
+def attainable_proj_seconds(hist, width, d, V, dtype, peak_tflops):
+    """Roofline bound of the projection over one decode: per step the larger
+    of its MFMA time (2 d |V| flops per row at peak) and the time to stream
+    W_out once from HBM; steps taken from the rows histogram at bucket
+    midpoints."""
+    es = 2 if dtype == "bf16" else 4
+    w_bytes = ((V + 127) // 128) * 128 * d * es
+    t = 0.0
+    for i, c in enumerate(hist):
+        if c:
+            rows = max(1.0, i * width + (width - 1) / 2.0)
+            t += c * max(2.0 * d * V * rows / (peak_tflops * 1e12), w_bytes / HBM_PEAK_BPS)
+    return t
 # Sources of the projection kernel; measured HBM traffic is reported only
 # while they are unchanged since the counters were taken.
 PROJ_SOURCES = ["paper_2010_02164_amd/csrc/proj.hip", "paper_2010_02164_amd/csrc/topk.h",
@@ -196,6 +212,8 @@ def main():
     proj_flops = 2.0 * cfg.d * cfg.V * st["expansions"] * args.steps
     achieved = proj_flops / (proj_ms * 1e-3) / 1e12 if proj_ms > 0 else 0.0
     peak = PEAK_TFLOPS[cfg.dtype]
+    t_att = attainable_proj_seconds(hist, hist_w, cfg.d, cfg.V, cfg.dtype, peak)
+    proj_s_per_decode = proj_ms * 1e-3 / args.steps
     workload_key = f"cfg{args.config} {args.sched} eps={eps:g}" + (f" pool={pool}" if pool else "")
     out = {
         "metric": METRIC, "value": hyps_per_s, "unit": "hyps/s", "n_gpus": 1,
@@ -209,7 +227,9 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "k_proj (vocabulary projection + log-sum-exp + top-k)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": measured_traffic(workload_key), "launches": proj_launches,
-                     "avg_launch_us": proj_ms * 1e3 / max(proj_launches, 1)},
+                     "avg_launch_us": proj_ms * 1e3 / max(proj_launches, 1),
+                     "attainable_ms_per_decode": t_att * 1e3,
+                     "frac_of_attainable": t_att / proj_s_per_decode if proj_s_per_decode > 0 else None},
         "rows_per_step_hist": {"bucket_width": hist_w,
                                "counts": {str(i * hist_w): c for i, c in enumerate(hist) if c}},
         "projection_share_of_step": (proj_ms * 1e-3) / elapsed if elapsed > 0 else None,
