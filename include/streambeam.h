@@ -135,7 +135,8 @@ typedef struct {
 
 /* One finalized hypothesis y_ij of Y[i] (Alg. 1 output). */
 typedef struct {
-  int64_t input;         /* queue position of its input (submission order)         */
+  int64_t input;         /* id of its input given to sb_submit (its queue position,
+                            in submission order, when no ids were given)         */
   int32_t rank;          /* position in Y[i]: rank order (0 = best) under the
                             paper's rule, finalization order under Fairseq's      */
   int32_t length;        /* number of tokens, EOS included when present            */
@@ -174,11 +175,12 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
                     size_t bytes, void *stream, sb_decoder **out);
 
 /* Append `count` inputs to the queue (Alg. 1's X, in index order).
- * h0: device [count][d] (dtype of the model), the encodings e_i = E(x_i),
- * copied asynchronously on the stream (the caller may reuse it once the
- * stream has passed this point). L_x, max_len: host [count], copied before
- * return; 1 <= max_len[i] <= max_len_cap. */
-sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_t *L_x,
+ * ids: host [count] caller ids echoed in sb_hyp.input, or NULL for the
+ * queue positions. h0: device [count][d] (dtype of the model), the
+ * encodings e_i = E(x_i), copied asynchronously on the stream (the caller
+ * may reuse it once the stream has passed this point). L_x, max_len: host
+ * [count], copied before return; 1 <= max_len[i] <= max_len_cap. */
+sb_status sb_submit(sb_decoder *dec, int32_t count, const int64_t *ids, const void *h0, const int32_t *L_x,
                     const int32_t *max_len);
 
 /* Enqueue one timestep of Alg. 1's loop (refill, select, expand, update,

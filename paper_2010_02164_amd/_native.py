@@ -79,7 +79,7 @@ def lib():
         "sb_workspace_bytes": (c_size_t, [P(SbModel), P(SbParams)]),
         "sb_validate": (c_int32, [P(SbModel), P(SbParams)]),
         "sb_create": (c_int32, [P(SbModel), P(SbParams), c_void_p, c_size_t, c_void_p, P(c_void_p)]),
-        "sb_submit": (c_int32, [c_void_p, c_int32, c_void_p, P(c_int32), P(c_int32)]),
+        "sb_submit": (c_int32, [c_void_p, c_int32, P(c_int64), c_void_p, P(c_int32), P(c_int32)]),
         "sb_step": (c_int32, [c_void_p, P(c_int32)]),
         "sb_run": (c_int32, [c_void_p]),
         "sb_collect": (c_int32, [c_void_p, P(SbHyp), c_int64, P(c_int32), c_int64, P(c_int64), P(c_int64)]),

@@ -38,6 +38,7 @@ struct sb_decoder {
   // projection launch, taken from this pool.
   std::vector<hipEvent_t> tev;
   int tev_used = 0;
+  std::vector<int64_t> ids;   // caller id per queue position
   std::string err;
 };
 
@@ -418,7 +419,7 @@ sb_status sb_reset(sb_decoder *dec) {
   return SB_OK;
 }
 
-sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_t *L_x,
+sb_status sb_submit(sb_decoder *dec, int32_t count, const int64_t *ids, const void *h0, const int32_t *L_x,
                     const int32_t *max_len) {
   if (!dec) return SB_E_INVALID_ARG;
   if (count < 0 || (count > 0 && (!h0 || !L_x || !max_len))) {
@@ -438,6 +439,8 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const void *h0, const int32_
     }
   }
   const int q0 = dec->n_queued;
+  if (dec->ids.size() < (size_t)p.max_inputs) dec->ids.resize(p.max_inputs);
+  for (int i = 0; i < count; ++i) dec->ids[q0 + i] = ids ? ids[i] : (int64_t)(q0 + i);
   const size_t es = dec->model.dtype == SB_BF16 ? 2 : 4;
   const size_t rowbytes = (size_t)dec->model.d * es;
   int32_t *lx = dec->pinned_len + q0;
@@ -556,7 +559,7 @@ sb_status sb_collect(sb_decoder *dec, sb_hyp *hyps, int64_t hyp_cap, int32_t *to
       for (int r = 0; r < c; ++r) {
         const OutHyp &o = oh[(size_t)(q - q0) * k + r];
         sb_hyp &y = hyps[h++];
-        y.input = q;
+        y.input = dec->ids[q];
         y.rank = r;
         y.length = o.length;
         y.status = o.status;

@@ -124,8 +124,10 @@ class Decoder:
         self._h0_keep = []
 
     # -- Alg. 1 calls ---------------------------------------------------------
-    def submit(self, h0, L_x: Sequence[int], max_len: Sequence[int]):
-        """Queue inputs: h0 is a device tensor [count, d] of the model dtype."""
+    def submit(self, h0, L_x: Sequence[int], max_len: Sequence[int], ids: Optional[Sequence[int]] = None):
+        """Queue inputs: h0 is a device tensor [count, d] of the model dtype;
+        ids (optional) are echoed as Hypothesis.input (default: queue
+        positions)."""
         torch = self.torch
         want = torch.bfloat16 if self.dtype == "bf16" else torch.float32
         if h0.dtype != want or not h0.is_cuda or h0.dim() != 2 or h0.shape[1] != self.d:
@@ -136,7 +138,13 @@ class Decoder:
         cnt = h0.shape[0]
         if lx.shape != (cnt,) or ml.shape != (cnt,):
             raise ValueError("L_x and max_len must have one entry per h0 row")
-        _check(N.lib().sb_submit(self.handle, cnt, ctypes.c_void_p(h0.data_ptr()),
+        idp = None
+        if ids is not None:
+            idv = np.ascontiguousarray(ids, dtype=np.int64)
+            if idv.shape != (cnt,):
+                raise ValueError("ids must have one entry per h0 row")
+            idp = idv.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+        _check(N.lib().sb_submit(self.handle, cnt, idp, ctypes.c_void_p(h0.data_ptr()),
                                  lx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                  ml.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))),
                "sb_submit", self.handle)

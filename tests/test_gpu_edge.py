@@ -75,3 +75,22 @@ def test_reuse_after_reset(gpu):
         dec.reset()
     torch.cuda.synchronize()
     dec.close()
+
+
+def test_caller_ids_are_echoed(gpu):
+    import torch
+    from paper_2010_02164_amd import decoder_for_workload, inputs_to_device
+    wl = make_workload(scaled(1, N=12))
+    ref, _, _ = gpu_decode(wl, "var_stream")
+    ids = 1000 + 7 * np.arange(12)
+    dec = decoder_for_workload(wl, sched="var_stream", max_inputs=12)
+    dec.submit(inputs_to_device(wl), wl.Lx, wl.max_len, ids=ids)
+    dec.run()
+    got = {}
+    for h in dec.collect():
+        got.setdefault(h.input, []).append((h.tokens, h.score, h.status))
+    assert sorted(got) == sorted(ids.tolist())
+    for i, y in enumerate(ref):
+        assert got[int(ids[i])] == [(h.tokens, h.score, h.status) for h in y]
+    torch.cuda.synchronize()
+    dec.close()
