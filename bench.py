@@ -126,6 +126,40 @@ def copy_calibration(nbytes, reps=5):
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
+def unfused_reference(cfg_i, rows_list, reps=20):
+    """Times the unfused alternative to the fused projection on the same
+    shapes: a library GEMM writing the [R, |V|] logits to HBM, then a
+    log-softmax and a top-k over them (torch / hipBLASLt). Comparison only;
+    the decoder never takes this path."""
+    import torch
+    from synthgen import get_config, make_workload
+    cfg = get_config(cfg_i)
+    wl = make_workload(cfg, N=8)
+    dt = torch.bfloat16 if wl.is_bf16 else torch.float32
+    W = torch.from_numpy(wl.W_out).to("cuda", dtype=dt)
+    out = []
+    for R in rows_list:
+        h = torch.tanh(torch.randn(R, cfg.d, device="cuda")).to(dt)
+        def once():
+            z = (h @ W.T).float()
+            lp = torch.log_softmax(z, dim=1)
+            return torch.topk(lp, cfg.k, dim=1)
+        for _ in range(3):
+            once()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            once()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        out.append({"rows": R, "us": us, "logits_bytes": R * cfg.V * 4,
+                    "tflops": 2.0 * cfg.d * cfg.V * R / (us * 1e-6) / 1e12})
+    print(json.dumps({"unfused_reference": f"cfg{cfg_i}", "dtype": cfg.dtype, "V": cfg.V, "d": cfg.d,
+                      "k": cfg.k, "results": out}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +176,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph-replay", action="store_true",
                     help="skip the extra untimed graph-replay decodes (counter runs)")
+    ap.add_argument("--unfused", default=None, metavar="ROWS",
+                    help="only time the unfused torch alternative (GEMM + log-softmax + top-k) at these "
+                         "comma-separated row counts")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -152,6 +189,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.unfused:
+        unfused_reference(args.config, [int(x) for x in args.unfused.split(",")])
         return
 
     import torch
