@@ -94,3 +94,31 @@ def test_caller_ids_are_echoed(gpu):
         assert got[int(ids[i])] == [(h.tokens, h.score, h.status) for h in y]
     torch.cuda.synchronize()
     dec.close()
+
+
+def test_largest_rows_and_state(gpu):
+    # n*k = 65536 rows per step at most (n = 4096, k = 16) with d = 4096: the
+    # decode runs to completion and sampled inputs match the oracle decoding
+    # them alone (results are per input, Sec. 3).
+    from oracle.compare import compare
+    from oracle.search import decode_workload
+    wl = make_workload(scaled(1, N=4096, n=4096, k=16, M=16, V=512, d=4096, len_lo=3, len_hi=6))
+    g, st, dec = gpu_decode(wl, "var_stream")
+    dec.close()
+    assert st["finished"] == 4096 and st["hyps"] == sum(len(y) for y in g)
+    sample = [0, 2047, 4095]
+    hy, mm = [], []
+    for i in sample:
+        o = decode_workload(wl, inputs=[i])
+        hy.append(o.hyps[0])
+        mm.append(o.min_margin[0])
+    rep = compare(hy, mm, [[(h.tokens, h.score, h.status) for h in g[i]] for i in sample], inputs=sample)
+    print(f"[parity] n=4096 k=16 d=4096 sampled: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures
+
+
+def test_long_outputs(gpu):
+    # Outputs of about 300 tokens (max_len 400): deep backpointer histories.
+    wl = make_workload(scaled(1, N=6, n=4, V=64, d=64, len_lo=290, len_hi=310, max_len=400))
+    rep, g, st, o = check_parity(wl, "var_stream")
+    assert max(len(h.tokens) for y in g for h in y) > 250
