@@ -111,7 +111,9 @@ __device__ __forceinline__ float recompute_logit(const DevState &st, int row, in
 template <int KB, int TK>
 __device__ __forceinline__ double merge_row(const DevState &st, int row, int lane, int k, cand_key &mine) {
   constexpr int PW = part_width(TK);
-  constexpr int NBT = 4;   // partials in flight per lane
+  // Partials in flight per lane (full-length lists come with fewer than 64
+  // tiles, one per lane).
+  constexpr int NBT = TK == TILE_KEYS_SHORT ? 4 : 1;
   const float *base = st.part + (size_t)row * st.S * PW;
   float m = -INFINITY, s = 0.0f;
   TopK<KB> tk;
@@ -235,33 +237,15 @@ __device__ __forceinline__ bool ranks_above(double sa, int ka, double sb, int kb
   return sa > sb || (sa == sb && ka < kb);
 }
 
-// One stage of a wave-wide choice of the best (score, key) pair.
-template <int S>
-__device__ __forceinline__ void best_stage(double &bs, int &bk) {
-  const unsigned long long sbits = (unsigned long long)__double_as_longlong(bs);
-  unsigned long long sa, sb;
-  uint32_t ka, kb;
-  stage64<S>(sbits, sa, sb);
-  stage32<S>((uint32_t)bk, ka, kb);
-  const double xa = __longlong_as_double((long long)sa), xb = __longlong_as_double((long long)sb);
-  const bool b_wins = ranks_above(xb, (int)kb, xa, (int)ka);
-  bs = b_wins ? xb : xa;
-  bk = b_wins ? (int)kb : (int)ka;
-}
-
 constexpr int BEAM_THREADS = 512;
 constexpr int BEAM_WAVES = BEAM_THREADS / 64;
 constexpr int NO_KEY = 0x7FFFFFFF;
 
-// Draw the best remaining head (score, key) over the wave; every lane gets it.
-__device__ __forceinline__ void wave_best(double &bs, int &bk) {
-  best_stage<0>(bs, bk);
-  best_stage<1>(bs, bk);
-  best_stage<2>(bs, bk);
-  best_stage<3>(bs, bk);
-  best_stage<4>(bs, bk);
-  best_stage<5>(bs, bk);
-}
+// A candidate expansion of the per-beam ranking (16 bytes, one LDS read).
+struct Cand {
+  double score;
+  int key, pad;
+};
 
 template <int KB, int TK>
 __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
@@ -304,6 +288,10 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   __shared__ int npar[KMAX_SUPPORTED], ntok[KMAX_SUPPORTED], nstat[KMAX_SUPPORTED];
   __shared__ int opar[KMAX_SUPPORTED], otok[KMAX_SUPPORTED], ostat[KMAX_SUPPORTED];
   __shared__ int nw_sh, nact_sh, no_sh;
+  // Candidates (at most k KC list entries + k no-ops) and the ranks kept.
+  __shared__ Cand cand[KMAX_SUPPORTED * (KMAX_SUPPORTED + 1)];
+  __shared__ double r_score[2 * KMAX_SUPPORTED];
+  __shared__ int r_key[2 * KMAX_SUPPORTED];
   if (tid < k) {
     sl_status[tid] = my_status;
     sl_row[tid] = my_row;
@@ -330,56 +318,66 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   }
   __syncthreads();
 
-  if (wave == 0) {
-    // Each parent's expansions arrive sorted, so the ranking of all
-    // expansions (key: score, parent rank, token) is a k-way merge: lane
-    // p < k holds the head of parent p's list, lane k + p the no-op of a
-    // terminated parent p (paper rule only); each round takes the best head
-    // (wave maximum) and its lane advances. Lane r keeps the entry of rank r.
-    const bool is_list = lane < k, is_noop = !fairseq && lane >= k && lane < 2 * k;
-    const int p = is_list ? lane : lane - k;
-    const int pstat = (is_list || is_noop) ? sl_status[p] : SLOT_EMPTY;
-    int hp = 0;
-    bool noop_left = is_noop && (pstat == SLOT_EOS || pstat == SLOT_MAXLEN);
-    double hs = -INFINITY;
-    int hk = NO_KEY;
-    auto head = [&]() {
-      hs = -INFINITY;
-      hk = NO_KEY;
-      if (is_list && pstat == SLOT_ACTIVE && hp < KC) {
-        const int tok = ch_tok[p * KC + hp];
-        if (tok >= 0 && tok < st.V) {
-          hs = sl_score[p] + ch_lp[p * KC + hp];
-          hk = (p << 24) | (tok + 1);
-        }
-      } else if (noop_left) {
-        hs = sl_score[p];
-        hk = p << 24;
+  // Ranking of all expansions (key: score, parent rank, token; Sec. 2):
+  // thread c < C holds candidate c (parent c / KC's child c % KC, or, paper
+  // rule, the no-op of terminated parent c - k KC) and counts the valid
+  // candidates that rank above it; that count is its rank, all keys being
+  // distinct. Ranks below RM (k, or 2k under the Fairseq rule) are kept.
+  const int NCL = k * KC;
+  const int C = NCL + (fairseq ? 0 : k);
+  const int RM = fairseq ? 2 * k : k;
+  double cs = -INFINITY;
+  int ck = NO_KEY;
+  bool cv = false;
+  if (tid < NCL) {
+    const int p = tid / KC, j = tid - p * KC;
+    if (sl_status[p] == SLOT_ACTIVE) {
+      const int tok = ch_tok[p * KC + j];
+      if (tok >= 0 && tok < st.V) {
+        cs = sl_score[p] + ch_lp[p * KC + j];
+        ck = (p << 24) | (tok + 1);
+        cv = true;
       }
-    };
-    head();
+    }
+  } else if (tid < C) {
+    const int p = tid - NCL;
+    if (sl_status[p] == SLOT_EOS || sl_status[p] == SLOT_MAXLEN) {
+      cs = sl_score[p];
+      ck = p << 24;
+      cv = true;
+    }
+  }
+  // Records up to a multiple of 8; invalid ones (score -inf) rank below
+  // every valid candidate.
+  const int C8 = (C + 7) & ~7;
+  if (tid < C8) cand[tid] = Cand{cs, ck, 0};
+  const int nvalid = __syncthreads_count(cv);
+  if (cv) {
+    int rank = 0;
+    for (int c0 = 0; c0 < C8; c0 += 8) {
+      Cand o[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) o[u] = cand[c0 + u];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) rank += (int)((o[u].score > cs) | ((o[u].score == cs) & (o[u].key < ck)));
+    }
+    if (rank < RM) {
+      r_score[rank] = cs;
+      r_key[rank] = ck;
+    }
+  }
+  __syncthreads();
+
+  if (wave == 0) {
+    // Lane r < nfull holds the expansion of rank r.
+    const int nfull = min(RM, nvalid);
     double rs = -INFINITY;
     int rk = NO_KEY;
-    int nfull = 0;
+    if (lane < nfull) {
+      rs = r_score[lane];
+      rk = r_key[lane];
+    }
     if (!fairseq) {
-      // Full beam B' (Sec. 2): the best k expansions, no-ops included.
-#pragma unroll 1
-      for (int r = 0; r < k; ++r) {
-        double bs = hs;
-        int bk = hk;
-        wave_best(bs, bk);
-        if (bk == NO_KEY) break;   // fewer than k candidates
-        if (lane == r) {
-          rs = bs;
-          rk = bk;
-        }
-        nfull = r + 1;
-        if (hk == bk) {            // the winner's lane advances
-          if (is_list) ++hp;
-          else noop_left = false;
-          head();
-        }
-      }
       // Heuristics H (Sec. 4) on B' in rank order: drop x if
       // score(x) < best - delta, best = B'[0] (possibly terminated,
       // App. A.3); drop an expansion whose parent already has M kept
@@ -420,26 +418,6 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
       // Fairseq rule (App. A.1): a terminated expansion among the best k is
       // output at once (until k outputs); the new beam is the first k
       // active expansions in rank order. Both lie within the first 2k ranks.
-      int nact = 0;
-#pragma unroll 1
-      for (int r = 0; r < 2 * k; ++r) {
-        double bs = hs;
-        int bk = hk;
-        wave_best(bs, bk);
-        if (bk == NO_KEY) break;
-        if (lane == r) {
-          rs = bs;
-          rk = bk;
-        }
-        nfull = r + 1;
-        const int wtok = (bk & 0xFFFFFF) - 1;
-        nact += !(wtok == 0 || t == max_len);
-        if (hk == bk) {
-          ++hp;
-          head();
-        }
-        if (nfull >= k && nact >= k) break;
-      }
       const int rpar = rk >> 24, rtok = (rk & 0xFFFFFF) - 1;
       const bool valid = lane < nfull;
       const bool term = valid && (rtok == 0 || t == max_len);
