@@ -135,18 +135,58 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
         rec[u][4 * x + 3] = __uint_as_float(v.w);
       }
     }
+    if constexpr (TK == TILE_KEYS_SHORT && NBT == 4) {
+      // Four sorted 4-key runs (empty past the last tile) merged by
+      // bitonic networks into the batch's best KB, then into the list.
+      TopK<4> run[4];
 #pragma unroll
-    for (int u = 0; u < NBT; ++u) {
-      if (t0 + 64 * u < st.S) {
-        TopK<TK> t4;
-        topk_load(t4, rec[u] + 2);
-        TopK<KB> o;
-        topk_init(o);
+      for (int u = 0; u < NBT; ++u) {
+        const bool ok = t0 + 64 * u < st.S;
+        topk_load(run[u], rec[u] + 2);
 #pragma unroll
-        for (int j = 0; j < TK; ++j) o.k[j] = t4.k[j];
-        lse_merge(m, s, rec[u][0], rec[u][1]);
-        last_max = t4.k[TK - 1] > last_max ? t4.k[TK - 1] : last_max;
-        topk_merge(tk, o);
+        for (int j = 0; j < 4; ++j) run[u].k[j] = ok ? run[u].k[j] : 0ull;
+        if (ok) lse_merge(m, s, rec[u][0], rec[u][1]);
+        last_max = run[u].k[3] > last_max ? run[u].k[3] : last_max;
+      }
+      TopK<KB> batch;
+      if constexpr (KB == 4) {
+        topk_merge(run[0], run[1]);
+        topk_merge(run[2], run[3]);
+        topk_merge(run[0], run[2]);
+        batch = run[0];
+      } else {
+        cand_key a8[8], b8[8];
+        merge_sorted<4>(run[0].k, run[1].k, a8);
+        merge_sorted<4>(run[2].k, run[3].k, b8);
+        if constexpr (KB == 8) {
+          TopK<8> x, y;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            x.k[j] = a8[j];
+            y.k[j] = b8[j];
+          }
+          topk_merge(x, y);
+          batch = x;
+        } else {
+          merge_sorted<8>(a8, b8, batch.k);
+        }
+      }
+      if (t0 == lane) tk = batch;
+      else topk_merge(tk, batch);
+    } else {
+#pragma unroll
+      for (int u = 0; u < NBT; ++u) {
+        if (t0 + 64 * u < st.S) {
+          TopK<TK> t4;
+          topk_load(t4, rec[u] + 2);
+          TopK<KB> o;
+          topk_init(o);
+#pragma unroll
+          for (int j = 0; j < TK; ++j) o.k[j] = t4.k[j];
+          lse_merge(m, s, rec[u][0], rec[u][1]);
+          last_max = t4.k[TK - 1] > last_max ? t4.k[TK - 1] : last_max;
+          topk_merge(tk, o);
+        }
       }
     }
   }

@@ -48,6 +48,22 @@ __device__ __forceinline__ void cex(cand_key &a, cand_key &b, bool desc) {
   b = y;
 }
 
+// out <- the 2N keys of a and b (each sorted best first) sorted best first:
+// a followed by b reversed is bitonic, and half-cleaners sort it.
+template <int N>
+__device__ __forceinline__ void merge_sorted(const cand_key *a, const cand_key *b, cand_key *out) {
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    out[j] = a[j];
+    out[N + j] = b[N - 1 - j];
+  }
+#pragma unroll
+  for (int st = N; st > 0; st >>= 1)
+#pragma unroll
+    for (int j = 0; j < 2 * N; ++j)
+      if ((j & st) == 0) cex(out[j], out[j + st], true);
+}
+
 // Sort N keys (N a power of two) best first with a bitonic network.
 template <int N>
 __device__ __forceinline__ void bitonic_sort_desc(cand_key *a) {
