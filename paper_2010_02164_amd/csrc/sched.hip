@@ -5,13 +5,15 @@
 // iteration space; Sec. 3's selection up to a limit on total beam width).
 // One workgroup; the step's decisions are taken on the device so no host
 // round trip is needed.
+#include <algorithm>
+
 #include "sb_internal.h"
 
 namespace sb {
 
 namespace {
 
-constexpr int SCHED_THREADS = 1024;
+constexpr int SCHED_THREADS = 1024;   // at most; a launch takes one wave per 64 x PER beams
 
 // Exclusive prefix sum across the workgroup; *total receives the sum.
 __device__ int block_excl_scan(int v, int *sm, int *total) {
@@ -112,7 +114,7 @@ __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *
   // The cut: l* = the first l_t whose cumulative width exceeds the budget;
   // every beam below l* fits, none above it is taken.
   const int L = st.max_len_cap, budget = st.row_budget;
-  const int bins = (L + SCHED_THREADS - 1) / SCHED_THREADS;
+  const int bins = (L + (int)blockDim.x - 1) / (int)blockDim.x;
   const int j0 = min(L, (int)threadIdx.x * bins), j1 = min(L, j0 + bins);
   int hsum = 0;
   for (int j = j0; j < j1; ++j) hsum += cs.hist[j];
@@ -157,11 +159,12 @@ __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *
 // row offsets with the step's totals.
 template <int PER>
 __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
-  constexpr int NW = SCHED_THREADS / 64;
-  __shared__ long long ph1[NW + 1];
-  __shared__ int ph1_min[NW + 1];
-  __shared__ int ph2[4][NW + 1];
-  __shared__ int sm[NW + 1];
+  constexpr int NWMAX = SCHED_THREADS / 64;
+  const int NW = (int)blockDim.x >> 6;
+  __shared__ long long ph1[NWMAX + 1];
+  __shared__ int ph1_min[NWMAX + 1];
+  __shared__ int ph2[4][NWMAX + 1];
+  __shared__ int sm[NWMAX + 1];
   __shared__ CapSmem cs;
   DevCtrl *c = st.ctrl;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -184,7 +187,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
         if (st.b_input[r] >= 0) orec[u] = r;
       }
     }
-    for (int j = tid; j < st.max_len_cap; j += SCHED_THREADS) cs.hist[j] = 0;
+    for (int j = tid; j < st.max_len_cap; j += (int)blockDim.x) cs.hist[j] = 0;
     if (tid == 0) {
       cs.cut[0] = INT_MAX;
       cs.cut[1] = 0;
@@ -431,9 +434,13 @@ __global__ void k_init(DevState st) {
 
 hipError_t launch_sched(const DevState &st, hipStream_t s) {
   const int per = (st.n + SCHED_THREADS - 1) / SCHED_THREADS;
-  if (per <= 1) hipLaunchKernelGGL(k_sched<1>, dim3(1), dim3(SCHED_THREADS), 0, s, st);
-  else if (per == 2) hipLaunchKernelGGL(k_sched<2>, dim3(1), dim3(SCHED_THREADS), 0, s, st);
-  else hipLaunchKernelGGL(k_sched<4>, dim3(1), dim3(SCHED_THREADS), 0, s, st);
+  // One wave per 64 x PER beam records (cross-wave scans and barriers then
+  // span only the waves that hold beams).
+  const int p = per <= 1 ? 1 : per == 2 ? 2 : 4;
+  const int threads = std::min(SCHED_THREADS, (st.n + 64 * p - 1) / (64 * p) * 64);
+  if (p == 1) hipLaunchKernelGGL(k_sched<1>, dim3(1), dim3(threads), 0, s, st);
+  else if (p == 2) hipLaunchKernelGGL(k_sched<2>, dim3(1), dim3(threads), 0, s, st);
+  else hipLaunchKernelGGL(k_sched<4>, dim3(1), dim3(threads), 0, s, st);
   return hipGetLastError();
 }
 
