@@ -88,10 +88,13 @@ def beam_step(beam: List[Cand], lp: dict, h_new: dict, t: int, max_len: int,
     full = pool[:k]
 
     # Margins of every ranking decision: adjacent pairs inside the full beam
-    # and the k-th vs (k+1)-th; the threshold boundary is added below.
+    # and the k-th vs (k+1)-th; the threshold boundary is added below. An
+    # exact tie is decided by parent rank and token, not by the scores, so it
+    # is no decision margin.
     margin = np.inf
     for a, b in zip(pool[:k], pool[1:k + 1]):
-        margin = min(margin, a[0] - b[0])
+        if a[0] != b[0]:
+            margin = min(margin, a[0] - b[0])
 
     # Heuristics H (Sec. 4): relative threshold delta, then max M per parent.
     ref = full[0][0]
@@ -159,7 +162,8 @@ def beam_step_fairseq(beam: List[Cand], lp: dict, h_new: dict, t: int, max_len: 
     margin = np.inf
     head = pool[:2 * k + 1]
     for a, b in zip(head, head[1:]):
-        margin = min(margin, a[0] - b[0])
+        if a[0] != b[0]:   # an exact tie is decided by parent rank and token
+            margin = min(margin, a[0] - b[0])
 
     def terminated(w):
         return w == eos or t == max_len
