@@ -40,13 +40,26 @@ __device__ __forceinline__ cand_key wave_max_key(cand_key x) {
 }
 
 // Wave-wide log-sum-exp combine of (max, sum exp) pairs; every lane ends
-// with the same result (each stage combines two disjoint lane sets with a
-// commutative merge).
+// with the same result. The merge is not symmetric in its operands once
+// the compiler fuses a product into the sum, so both lanes of a pair take
+// them in the same order: the lower lane's first (the swap stages 4 and 5
+// already hand both lanes the pair in that order).
 template <int S>
 __device__ __forceinline__ void lse_stage(float &m, float &s) {
   uint32_t ma, mb, sa, sb;
   stage32<S>(__float_as_uint(m), ma, mb);
   stage32<S>(__float_as_uint(s), sa, sb);
+  if constexpr (S <= 3) {
+    const int lane = (int)(threadIdx.x & 63);
+    const bool lower = S == 0 ? !(lane & 1) : S == 1 ? !(lane & 2) : S == 2 ? (lane & 7) < 4 : (lane & 15) < 8;
+    if (!lower) {
+      const uint32_t tm = ma, ts = sa;
+      ma = mb;
+      sa = sb;
+      mb = tm;
+      sb = ts;
+    }
+  }
   float M = __uint_as_float(ma), Sm = __uint_as_float(sa);
   lse_merge(M, Sm, __uint_as_float(mb), __uint_as_float(sb));
   m = M;
@@ -204,7 +217,9 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
       tk.k[KB - 1] = 0ull;
     }
   }
-  if (__ballot(last_max > kth) == 0ull) return (double)m + log((double)s);
+  // The row's log-sum-exp as lane 0 has it, for every lane.
+  const double lse = __shfl((double)m + log((double)s), 0, 64);
+  if (__ballot(last_max > kth) == 0ull) return lse;
 
   // Rare path: rebuild the lists with the saturated tiles recomputed.
   topk_init(tk);
@@ -250,7 +265,7 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
       tk.k[KB - 1] = 0ull;
     }
   }
-  return (double)m + log((double)s);
+  return lse;
 }
 
 // Row merge as its own kernel (wave per row), for the single-expansion

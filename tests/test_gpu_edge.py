@@ -122,3 +122,33 @@ def test_long_outputs(gpu):
     wl = make_workload(scaled(1, N=6, n=4, V=64, d=64, len_lo=290, len_hi=310, max_len=400))
     rep, g, st, o = check_parity(wl, "var_stream")
     assert max(len(h.tokens) for y in g for h in y) > 250
+
+
+def _plant_ties(wl, pairs):
+    # Tokens 2j+1 and 2j+2 share their output and embedding rows: their
+    # logits are equal, and so are the states and scores of two children
+    # that differ only in them, at every later step. Such exact ties are
+    # decided by the ranking key alone (parent rank, then token), and the
+    # oracle logs them as no decision margin, so these inputs are compared
+    # strictly.
+    for a in range(1, 2 * pairs, 2):
+        wl.W_out[a + 1] = wl.W_out[a]
+        wl.E[a + 1] = wl.E[a]
+
+
+@pytest.mark.parametrize("cfg_i,over,pairs,sched,kw", [
+    (1, dict(N=24), 200, "var_stream", {}),
+    (1, dict(N=24), 200, "fixed", {}),
+    (1, dict(N=24), 200, "fixed_fairseq", {}),
+    (1, dict(N=24), 200, "var_cap", dict(pool=16)),
+    (4, dict(N=24, n=8, V=4000, d=256, len_hi=20), 600, "var_stream", {}),
+])
+def test_exact_ties_follow_rank_key(gpu, cfg_i, over, pairs, sched, kw):
+    # Small vocabularies: every tile keeps the full key list, so no tile is
+    # recomputed and every logit comes from the projection kernel.
+    wl = make_workload(scaled(cfg_i, **over))
+    _plant_ties(wl, pairs)
+    rep, g, st, o = check_parity(wl, sched, **kw)
+    tied = sum(1 for y in o.hyps for i in range(len(y)) for j in range(i + 1, len(y)) if y[i].score == y[j].score)
+    assert tied > 0                                  # the ties reach the outputs
+    assert rep.n_excused <= rep.n_inputs // 3        # most inputs compared strictly
