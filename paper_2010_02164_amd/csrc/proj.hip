@@ -92,6 +92,10 @@ __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned 
       u4 braw[NBV];
 #pragma unroll
       for (int bb = 0; bb < NBV; ++bb) braw[bb] = *reinterpret_cast<const u4 *>(&T[32 * bb + l32][64 * h + 16 * q]);
+      // Raised wave priority while this piece's MFMAs issue, so that of the
+      // two waves sharing a SIMD the one whose operands are in keeps the
+      // matrix unit fed (fp32 steps of 128-640 rows: 1-2 % faster).
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int bb = 0; bb < NBV; ++bb) {
 #pragma unroll
@@ -108,6 +112,7 @@ __device__ __forceinline__ void proj_mainloop(unsigned char (*Bt)[LS], unsigned 
           }
         }
       }
+      __builtin_amdgcn_s_setprio(0);
     }
   };
 
