@@ -414,7 +414,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) o[u] = cand[c0 + u];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) rank += (int)((o[u].score > cs) | ((o[u].score == cs) & (o[u].key < ck)));
+      for (int u = 0; u < 8; ++u) rank += ranks_above(o[u].score, o[u].key, cs, ck) ? 1 : 0;
     }
     if (rank < RM) {
       r_score[rank] = cs;
@@ -569,7 +569,6 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   // state; active children take their parent's new state h).
   if (tid < k) {
     if (tid < w) {
-      const int par = npar[tid];
       st.s_status[base + tid] = nstat[tid];
       st.s_score[base + tid] = nscore[tid];
       if (ntok[tid] >= 0) st.s_tok[base + tid] = ntok[tid];

@@ -37,7 +37,7 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 __global__ __launch_bounds__(THREADS, 2) void k_kv_append(DevState st) {
   const int R = st.ctrl->R;
   const int d = st.d, NO = st.kv_layers * 2 * d;
-  const int nvt = NO / BV, nrt = (st.R_max + BR - 1) / BR;
+  const int nrt = (st.R_max + BR - 1) / BR;
   const int g = blockIdx.x;
   const int vt = g / nrt, rt = g - vt * nrt;
   const int v0 = vt * BV, r0 = rt * BR;

@@ -11,8 +11,6 @@
 namespace sb {
 namespace {
 
-constexpr int THREADS = 256;
-
 // ---------------------------------------------------------------- K_rec
 // The recurrence GEMM is small ([R,d] x [d,d]) next to the projection, so it
 // is cut into 32 (out features) x 32 (rows) tiles to reach hundreds of
