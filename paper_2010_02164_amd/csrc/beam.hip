@@ -75,7 +75,13 @@ __device__ __forceinline__ void wave_lse(float &m, float &s) {
 }
 
 // Logit z[v] of one row recomputed from W_out and the row's projection
-// input (fp32 accumulation), with the EOS bias of token 0.
+// input (fp32 accumulation), with the EOS bias of token 0. fp32 follows the
+// projection's arithmetic exactly: each K half in chunks of 32 values, and
+// per chunk, piece q and element e the two fused products of k and k + 16
+// (an fp32 32x32x2 MFMA adds its two products to the sum one after the
+// other, lane half 0's first), then the halves added once, so a recomputed
+// logit equals the projection's bit for bit. bf16 sums the same products
+// in plain order (the bf16 MFMA's internal rounding is not reproduced).
 __device__ __forceinline__ float recompute_logit(const DevState &st, int row, int v) {
   const int d = st.d;
   float z = 0.0f;
@@ -92,15 +98,21 @@ __device__ __forceinline__ float recompute_logit(const DevState &st, int row, in
       }
     }
   } else {
-    const float4 *w = reinterpret_cast<const float4 *>(static_cast<const float *>(st.W_out) + (size_t)v * d);
-    const float4 *x = reinterpret_cast<const float4 *>(static_cast<const float *>(st.proj_in) + (size_t)row * d);
-    for (int c = 0; c < d / 4; ++c) {
-      const float4 a = w[c], b = x[c];
-      z = fmaf(a.x, b.x, z);
-      z = fmaf(a.y, b.y, z);
-      z = fmaf(a.z, b.z, z);
-      z = fmaf(a.w, b.w, z);
+    const float *w = static_cast<const float *>(st.W_out) + (size_t)v * d;
+    const float *x = static_cast<const float *>(st.proj_in) + (size_t)row * d;
+    float half[2];
+    for (int g = 0; g < 2; ++g) {
+      float acc = 0.0f;
+      for (int c = g * (d / 2); c < (g + 1) * (d / 2); c += 32)
+        for (int q = 0; q < 4; ++q)
+          for (int e = 0; e < 4; ++e) {
+            const int k0 = c + 4 * q + e;
+            acc = fmaf(w[k0], x[k0], acc);
+            acc = fmaf(w[k0 + 16], x[k0 + 16], acc);
+          }
+      half[g] = acc;
     }
+    z = half[0] + half[1];
   }
   if (v == 0) z += st.beta * (float)(st.r_t[row] - st.r_Lx[row]);
   return z;

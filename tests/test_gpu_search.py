@@ -152,3 +152,19 @@ def test_tile_list_completion(gpu, cfg):
     wl = _clustered(cfg)
     rep, g, st, o = check_parity(wl, "var_stream")
     assert st["tile_recomputes"] > 0
+
+
+def test_recomputed_tiles_tie_exactly(gpu):
+    # fp32: tokens 201 and 202 (second tile) copy the output and embedding
+    # rows of tokens 3 and 5 in the clustered first tile, which the row merge
+    # recomputes. A recomputed logit equals the projection's bit for bit, so
+    # the exact ties between a token and its copy (and later between the
+    # siblings they start) are decided by the ranking key, as in the oracle.
+    wl = _clustered(scaled(1, N=40, k=8, M=8, V=8192))
+    for a, b in ((3, 201), (5, 202)):
+        wl.W_out[b] = wl.W_out[a]
+        wl.E[b] = wl.E[a]
+    rep, g, st, o = check_parity(wl, "var_stream")
+    assert st["tile_recomputes"] > 0
+    tied = sum(1 for y in o.hyps for i in range(len(y)) for j in range(i + 1, len(y)) if y[i].score == y[j].score)
+    assert tied > 0
