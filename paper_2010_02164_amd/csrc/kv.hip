@@ -7,15 +7,11 @@
 // candidate, and a candidate reaches its rows through the ranks of its
 // ancestors per level, which the beam update passes on (a few bytes per
 // child instead of 2 L d t bytes).
-#include "sb_internal.h"
+#include "mfma_common.h"
 
 namespace sb {
 namespace {
 
-typedef float f16v __attribute__((ext_vector_type(16)));
-typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
-typedef unsigned int u4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u2 __attribute__((ext_vector_type(2)));
 
 constexpr int THREADS = 256;
 constexpr int BV = GEMM_BV, BR = GEMM_BR;
@@ -37,9 +33,10 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 __global__ __launch_bounds__(THREADS, 2) void k_kv_append(DevState st) {
   const int R = st.ctrl->R;
   const int d = st.d, NO = st.kv_layers * 2 * d;
-  const int nrt = (st.R_max + BR - 1) / BR;
-  const int g = blockIdx.x;
-  const int vt = g / nrt, rt = g - vt * nrt;
+  // XCD-aware order: the row tiles of one W_kv column tile run on one XCD
+  // and share its L2 copy of the tile.
+  int vt, rt;
+  if (!tile_of(NO / BV, (st.R_max + BR - 1) / BR, vt, rt)) return;
   const int v0 = vt * BV, r0 = rt * BR;
   if (r0 >= R) return;
   __shared__ Smem sm;
@@ -120,7 +117,7 @@ __global__ void k_transpose(const uint16_t *W, uint16_t *WT, int L2, int d) {
 
 hipError_t launch_kv_append(const DevState &st, hipStream_t s) {
   const int NO = st.kv_layers * 2 * st.d;
-  const int G = (NO / BV) * ((st.R_max + BR - 1) / BR);
+  const int G = xcd_grid((NO / BV) * ((st.R_max + BR - 1) / BR));
   hipLaunchKernelGGL(k_kv_append, dim3(G), dim3(THREADS), 0, s, st);
   return hipGetLastError();
 }
