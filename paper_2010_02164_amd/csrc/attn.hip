@@ -61,7 +61,7 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 
 // d = 256 E. Lane l of wave w owns columns w d/4 + l E .. + E - 1 (the V
 // pass), and for the K pass the four pieces p d/4 + l E .. + E - 1.
-// Persistent over the R*L (row, layer) pairs, layer minor.
+// Persistent over the R*L (row, layer) pairs.
 template <int E>
 __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
   extern __shared__ double sc[];   // [max_len_cap] scores, then weights; then the ranks
@@ -74,8 +74,14 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
   uint8_t *arank = reinterpret_cast<uint8_t *>(sc + st.max_len_cap);   // [max_len_cap]
   const uint16_t *hb = static_cast<const uint16_t *>(st.hbuf);
 
-  for (int pr = blockIdx.x; pr < R * L; pr += gridDim.x) {
-    const int r = pr / L, l = pr - r * L;
+  // Pairs in layer-major order (rows come in beam order, so the siblings
+  // that share ancestor rows are adjacent); XCD x walks the x-th eighth of
+  // the list, so siblings read those rows through one L2.
+  const int T = R * L;
+  const int xcd = blockIdx.x & 7, gx = gridDim.x >> 3;
+  const int lo = (int)((long long)T * xcd / 8), hi = (int)((long long)T * (xcd + 1) / 8);
+  for (int pr = lo + (int)(blockIdx.x >> 3); pr < hi; pr += gx) {
+    const int l = pr / R, r = pr - l * R;
     const int slot = st.r_slot[r];
     const int t = st.r_t[r];                         // positions, the new one included
     const int b = slot / k;
@@ -156,7 +162,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn(DevState st) {
 #pragma unroll
         for (int e = 0; e < E; ++e) a[e] = fma(ws, bf_to_d(c[e]), a[e]);
       }
-      double *out = st.attn_part + (size_t)pr * d + col;
+      double *out = st.attn_part + ((size_t)r * L + l) * d + col;
 #pragma unroll
       for (int e = 0; e < E; ++e) out[e] = a[e] / den;
       __syncthreads();   // sc, red and arank are rewritten by the next pair
@@ -194,7 +200,7 @@ __global__ __launch_bounds__(AT_THREADS) void k_attn_combine(DevState st) {
 }  // namespace
 
 hipError_t launch_attn(const DevState &st, hipStream_t s) {
-  const int G = std::min(st.R_max * st.kv_layers, st.n_cu * 8);
+  const int G = (std::min(st.R_max * st.kv_layers, st.n_cu * 8) + 7) / 8 * 8;   // a multiple of the 8 XCDs
   const size_t lds = (size_t)st.max_len_cap * (sizeof(double) + 1);
   switch (st.d) {
     case 256: hipLaunchKernelGGL(k_attn<1>, dim3(G), dim3(AT_THREADS), lds, s, st); break;
