@@ -75,6 +75,11 @@ def cpu_baseline(wl, sched, eps, sample, pool=None):
     except Exception:
         threads = 0
     cores = threads or len(os.sched_getaffinity(0))
+    try:
+        b = np.show_config(mode="dicts").get("Build Dependencies", {}).get("blas", {})
+        blas = f"{b.get('name', '?')} {b.get('version', '')}".strip()
+    except Exception:
+        blas = "unknown"
     idx = np.arange(min(sample, len(wl.Lx)))
     t0 = time.perf_counter()
     r = decode_workload(wl, sched=sched, eps=eps, inputs=idx, pool=pool)
@@ -82,7 +87,8 @@ def cpu_baseline(wl, sched, eps, sample, pool=None):
     return {"value": r.n_hyps / dt, "unit": "hyps/s", "cores": cores, "kind": "oracle",
             "sample": f"first {len(idx)} of {len(wl.Lx)} inputs, same n/k/eps/delta/M/pool, numpy fp64 "
                       f"({dt:.1f} s, {r.expansions} expansions)",
-            "expansions_per_s": r.expansions / dt, "seconds": dt}
+            "expansions_per_s": r.expansions / dt, "seconds": dt, "blas": blas, "blas_threads": threads or None,
+            "host_cpus": len(os.sched_getaffinity(0))}
 
 
 def proj_source_sha256():
