@@ -235,10 +235,13 @@ def main():
     dec.set_timing(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    run_ends = []
     for _ in range(args.steps):
-        run_once()
+        run_once()             # sb_run returns once the decode is complete on the device
+        run_ends.append(time.perf_counter())
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    run_ms = np.diff(np.array([t0] + run_ends)) * 1e3
     proj_ms, proj_launches = dec.timing()
     dec.set_timing(False)
     st = dec.stats()            # counters of the last run
@@ -271,6 +274,7 @@ def main():
     out = {
         "metric": METRIC, "value": hyps_per_s, "unit": "hyps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": per_run * 1e3,
+        "ms_per_step_std": float(run_ms.std(ddof=1)) if len(run_ms) > 1 else 0.0,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
         "config": {"workload": _workload_desc(cfg, args.sched, eps, pool) + (", inputs sorted by L_x" if args.sorted else ""), "key": workload_key, "inputs": N,
