@@ -168,3 +168,31 @@ def test_recomputed_tiles_tie_exactly(gpu):
     assert st["tile_recomputes"] > 0
     tied = sum(1 for y in o.hyps for i in range(len(y)) for j in range(i + 1, len(y)) if y[i].score == y[j].score)
     assert tied > 0
+
+
+def test_launch_modes_agree(gpu):
+    # One decode through captured step graphs (run), through per-kernel
+    # launches with the projection bracketed by events (the timed mode of
+    # bench.py) and through single synchronized steps: identical outputs,
+    # counters and rows histograms.
+    import torch
+    from paper_2010_02164_amd import decoder_for_workload, group_by_input, inputs_to_device
+    wl = make_workload(scaled(3, N=24, n=8, V=8000))
+    key = lambda ys: [[(h.tokens, h.score, h.status) for h in y] for y in ys]
+    outs = []
+    for mode in ("graph", "timed", "step"):
+        dec = decoder_for_workload(wl, sched="var_stream", max_inputs=24)
+        if mode == "timed":
+            dec.set_timing(True)
+        dec.submit(inputs_to_device(wl), wl.Lx, wl.max_len)
+        if mode == "step":
+            for _ in range(100000):
+                if dec.step(sync=True):
+                    break
+        else:
+            dec.run()
+        hist, width = dec.rows_histogram()
+        outs.append((key(group_by_input(dec.collect(), 24)), dec.stats(), list(hist), width))
+        dec.close()
+    torch.cuda.synchronize()
+    assert outs[0] == outs[1] == outs[2]
