@@ -304,8 +304,12 @@ __device__ __forceinline__ bool ranks_above(double sa, int ka, double sb, int kb
   return sa > sb || (sa == sb && ka < kb);
 }
 
+// Threads of a beam workgroup: 8 waves (a wave per parent row), or 4 waves
+// when the vocabulary has at most 8 tiles and a row's merge is short (four
+// workgroups then share a compute unit). Both hold a thread per candidate
+// of the ranking up to k = 15.
 constexpr int BEAM_THREADS = 512;
-constexpr int BEAM_WAVES = BEAM_THREADS / 64;
+constexpr int BEAM_THREADS_SMALL = 256;
 constexpr int NO_KEY = 0x7FFFFFFF;
 
 // A candidate expansion of the per-beam ranking (16 bytes, one LDS read).
@@ -314,8 +318,9 @@ struct Cand {
   int key, pad;
 };
 
-template <int KB, int TK>
-__global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
+template <int KB, int TK, int NT>
+__global__ __launch_bounds__(NT) void k_beam(DevState st) {
+  constexpr int BEAM_WAVES = NT / 64;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -600,7 +605,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
   const uint4 *__restrict__ hb = static_cast<const uint4 *>(st.hbuf);
   uint4 *__restrict__ sh = static_cast<uint4 *>(st.s_h);
   const int total = w * chunks;
-  for (int x = tid; x < total; x += BEAM_THREADS) {
+  for (int x = tid; x < total; x += NT) {
     const int r = x / chunks, c = x - r * chunks;
     if (nstat[r] == SLOT_ACTIVE) sh[(size_t)(base + r) * chunks + c] = hb[(size_t)sl_row[npar[r]] * chunks + c];
   }
@@ -612,7 +617,7 @@ __global__ __launch_bounds__(BEAM_THREADS) void k_beam(DevState st) {
     const uint32_t *src = reinterpret_cast<const uint32_t *>(st.anc) + ((size_t)apar * st.n * k + base) * A4;
     uint32_t *dst = reinterpret_cast<uint32_t *>(st.anc) + ((size_t)(apar ^ 1) * st.n * k + base) * A4;
     const int nw = (t - 1) / 4 + 1, last = (t - 1) / 4, sh8 = ((t - 1) & 3) * 8;
-    for (int x = tid; x < w * nw; x += BEAM_THREADS) {
+    for (int x = tid; x < w * nw; x += NT) {
       const int r = x / nw, wi = x - r * nw;
       if (nstat[r] != SLOT_ACTIVE) continue;
       uint32_t v = src[(size_t)npar[r] * A4 + wi];
@@ -675,17 +680,24 @@ hipError_t launch_rowmerge(const DevState &st, hipStream_t s) {
 
 hipError_t launch_beam(const DevState &st, hipStream_t s) {
   const bool sh = st.tile_keys == TILE_KEYS_SHORT;
+  const bool small = st.S <= 8 && st.k <= 15;   // short row merges: 4-wave workgroups
+#define SB_BEAM(KB, TK)                                                                               \
+  do {                                                                                                \
+    if (small) hipLaunchKernelGGL((k_beam<KB, TK, BEAM_THREADS_SMALL>), dim3(st.n), dim3(BEAM_THREADS_SMALL), 0, s, st); \
+    else hipLaunchKernelGGL((k_beam<KB, TK, BEAM_THREADS>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); \
+  } while (0)
   switch (st.kbucket) {
-    case 4: hipLaunchKernelGGL((k_beam<4, 4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st); break;
+    case 4: SB_BEAM(4, 4); break;
     case 8:
-      if (sh) hipLaunchKernelGGL((k_beam<8, 4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
-      else hipLaunchKernelGGL((k_beam<8, 8>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+      if (sh) SB_BEAM(8, 4);
+      else SB_BEAM(8, 8);
       break;
     default:
-      if (sh) hipLaunchKernelGGL((k_beam<16, 4>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
-      else hipLaunchKernelGGL((k_beam<16, 16>), dim3(st.n), dim3(BEAM_THREADS), 0, s, st);
+      if (sh) SB_BEAM(16, 4);
+      else SB_BEAM(16, 16);
       break;
   }
+#undef SB_BEAM
   return hipGetLastError();
 }
 
