@@ -180,8 +180,11 @@ __global__ __launch_bounds__(RTHREADS) void k_rec(DevState st) {
 }  // namespace
 
 hipError_t launch_rec(const DevState &st, hipStream_t s) {
-  // Multiple of 8; two workgroups per compute unit at most.
-  const int G = std::max(8, std::min(st.n_cu / 4 * 8, xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT))));
+  // Multiple of 8, no more than the tiles of a full step, and at most the
+  // workgroups that fit on the device at once: two per compute unit for
+  // bf16 (64 KB of LDS each), four for fp32 (32 KB).
+  const int tiles = xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT));
+  const int G = std::max(8, std::min(st.n_cu / (st.dtype == 1 ? 4 : 2) * 8, tiles));
   if (st.dtype == 1)
     hipLaunchKernelGGL(k_rec<true>, dim3(G), dim3(RTHREADS), 0, s, st);
   else
