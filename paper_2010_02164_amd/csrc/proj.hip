@@ -637,8 +637,10 @@ __global__ void k_relayout_wout(const unsigned char *__restrict__ src, unsigned 
 
 template <bool BF16>
 hipError_t launch_proj_t(const DevState &st, hipStream_t s) {
-  // Multiple of 8, at most one per compute unit, no more than the tiles of a full step.
-  const int G = std::max(8, std::min(st.n_cu / 8 * 8, xcd_grid(st.S * ((st.R_max + TR - 1) / TR))));
+  // Multiple of 8, at most one per compute unit, no more than the 32-row
+  // tiles of a full step (a small vocabulary then still spreads a large step
+  // over the device).
+  const int G = std::max(8, std::min(st.n_cu / 8 * 8, xcd_grid(st.S * ((st.R_max + 31) / 32))));
   switch (st.tile_keys) {
     case 4: hipLaunchKernelGGL((k_proj<BF16, 4>), dim3(G), dim3(THREADS), 0, s, st); break;
     case 8: hipLaunchKernelGGL((k_proj<BF16, 8>), dim3(G), dim3(THREADS), 0, s, st); break;
