@@ -64,13 +64,12 @@ struct CapSmem {
 // Capacity-constrained selection (Sec. 3, last paragraph): the live beams
 // in order of (l_t, admission) are taken while their active candidates total
 // at most row_budget rows. Called by the whole workgroup after admission
-// with the thread's records (inp, stp) and its kept positions of the old
-// order list (orec); nlive = live beams after admission. Leaves cs.sel[b]
+// with the thread's records (inp, stp, active-slot masks) and its kept
+// positions of the old order list (orec); nlive = live beams after admission. Leaves cs.sel[b]
 // set for the selected records and writes the new order list to b_order.
 template <int PER>
 __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *inp, const int *stp,
-                           const int *orec, int b0, int nb, int nlive) {
-  const int k = st.k;
+                           const uint32_t *amask, const int *orec, int b0, int nb, int nlive) {
   // Kept positions are compacted in order ahead of the admitted beams.
   int kept_l = 0;
 #pragma unroll
@@ -87,12 +86,7 @@ __device__ void cap_select(const DevState &st, CapSmem &cs, int *sm, const int *
       const int b = b0 + u;
       cs.sel[b] = 0;
       if (inp[u] >= 0) {
-        int w = 1;
-        if (stp[u] > 0) {
-          w = 0;
-          for (int j = 0; j < k; ++j) w += st.s_status[b * k + j] == SLOT_ACTIVE;
-        }
-        cs.info[b] = (stp[u] << 8) | w;
+        cs.info[b] = (stp[u] << 8) | __popc(amask[u]);   // a fresh beam: one candidate
       }
     }
   }
@@ -194,11 +188,14 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     }
   }
 
-  // Beam records, slot states (active / terminated masks) and, with one beam
-  // per thread, the slots' last tokens.
-  int inp[PER], stp[PER];
+  // Beam records, slot states (active / terminated masks), the inputs'
+  // source lengths and, with at most two beams per thread, the slots' last
+  // tokens. The slot loops run to the compile-time bound so that all loads
+  // are in flight together.
+  constexpr int PT = PER <= 2 ? PER : 1;
+  int inp[PER], stp[PER], lxv[PER];
   uint32_t amask[PER], tmask[PER];
-  int tok[PER == 1 ? KMAX_SUPPORTED : 1];
+  int tok[PT][KMAX_SUPPORTED];
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     inp[u] = -1;
@@ -208,17 +205,19 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     if (u < nb) {
       inp[u] = st.b_input[b0 + u];
       stp[u] = st.b_steps[b0 + u];
-      for (int j = 0; j < k; ++j) {
-        const int status = st.s_status[(b0 + u) * k + j];
-        amask[u] |= (uint32_t)(status == SLOT_ACTIVE) << j;
-        tmask[u] |= (uint32_t)(status == SLOT_EOS || status == SLOT_MAXLEN) << j;
+#pragma unroll
+      for (int j = 0; j < KMAX_SUPPORTED; ++j) {
+        if (j < k) {
+          const int status = st.s_status[(b0 + u) * k + j];
+          amask[u] |= (uint32_t)(status == SLOT_ACTIVE) << j;
+          tmask[u] |= (uint32_t)(status == SLOT_EOS || status == SLOT_MAXLEN) << j;
+          if (u < PT) tok[u < PT ? u : 0][j] = st.s_tok[(b0 + u) * k + j];
+        }
       }
     }
   }
-  if constexpr (PER == 1) {
-    if (nb > 0)
-      for (int j = 0; j < k; ++j) tok[j] = st.s_tok[b0 * k + j];
-  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) lxv[u] = inp[u] >= 0 ? st.q_Lx[inp[u]] : 0;
 
   // Phase 1: live (low word) and free (high word) records, exclusive over
   // threads, and the minimal l_t of the live beams.
@@ -279,7 +278,8 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
           stp[u] = 0;
           amask[u] = 1u;
           tmask[u] = 0u;
-          if constexpr (PER == 1) tok[0] = 0;
+          lxv[u] = st.q_Lx[inp[u]];
+          if (u < PT) tok[u < PT ? u : 0][0] = 0;
           st.b_input[b] = inp[u];
           st.b_steps[b] = 0;
           st.b_par[b] = 0;
@@ -302,7 +302,7 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
   // the beam with the most steps down, covers all of them), or the
   // capacity-constrained prefix.
   const int mn = admit > 0 ? 0 : mn0;
-  if (cap) cap_select<PER>(st, cs, sm, inp, stp, orec, b0, nb, live + admit);
+  if (cap) cap_select<PER>(st, cs, sm, inp, stp, amask, orec, b0, nb, live + admit);
 
   bool sel[PER];
   int act_l = 0, term_l = 0, sel_l = 0, pos_l = 0;
@@ -366,12 +366,14 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     if (u < nb) {
       const int b = b0 + u;
       st.b_sel[b] = sel[u];
-      const int lx = sel[u] ? st.q_Lx[inp[u]] : 0;
-      for (int j = 0; j < k; ++j) {
+      const int lx = sel[u] ? lxv[u] : 0;
+#pragma unroll
+      for (int j = 0; j < KMAX_SUPPORTED; ++j) {
+        if (j >= k) break;
         const int s = b * k + j;
         if ((amask[u] >> j) & 1u) {
           int y;
-          if constexpr (PER == 1) y = tok[j];
+          if (u < PT) y = tok[u < PT ? u : 0][j];
           else y = st.s_tok[s];
           st.r_slot[row] = s;
           st.r_hsrc[row] = stp[u] == 0 ? -1 - inp[u] : s;   // a fresh beam reads its encoding h0
@@ -394,16 +396,18 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
     c->n_sel = nsel;
     c->t_sel = R > 0 ? mn + 1 : 0;
     c->done = R == 0 ? 1 : 0;
+    // Counters by atomic adds whose results are not read (no wait).
+    typedef unsigned long long u64;
     if (R > 0) {
-      c->rows_hist[min(63, R / st.hist_width)] += 1;
-      c->timesteps += 1;
-      c->expansions += R;
-      c->noops += noops;
-      c->positions += npos;
+      atomicAdd(reinterpret_cast<u64 *>(&c->rows_hist[min(63, R / st.hist_width)]), 1ull);
+      atomicAdd(reinterpret_cast<u64 *>(&c->timesteps), 1ull);
+      atomicAdd(reinterpret_cast<u64 *>(&c->expansions), (u64)R);
+      atomicAdd(reinterpret_cast<u64 *>(&c->noops), (u64)noops);
+      atomicAdd(reinterpret_cast<u64 *>(&c->positions), (u64)npos);
     }
     if (admit > 0) {
-      c->refills += 1;
-      c->admitted += admit;
+      atomicAdd(reinterpret_cast<u64 *>(&c->refills), 1ull);
+      atomicAdd(reinterpret_cast<u64 *>(&c->admitted), (u64)admit);
     }
   }
 }
