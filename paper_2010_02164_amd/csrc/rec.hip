@@ -49,8 +49,23 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
   const int h = (lane >> 5) * 4;
   f16v acc = {};
   // K permutation: lanes 0-31 feed k = kk + e, lanes 32-63 k = kk + 4 + e.
+  // Blocks of 128 K values have all their loads issued before their MFMAs
+  // (the MFMA order is unchanged); the rest goes 8 at a time.
+  int kk = 0;
+  for (; kk + 128 <= kq; kk += 128) {
+    f4 a[16], b[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      a[i] = *reinterpret_cast<const f4 *>(arow + kk + 8 * i + h);
+      b[i] = *reinterpret_cast<const f4 *>(brow + kk + 8 * i + h);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[i][e], acc, 0, 0, 0);
+  }
 #pragma unroll 8
-  for (int kk = 0; kk < kq; kk += 8) {
+  for (; kk < kq; kk += 8) {
     const f4 a = *reinterpret_cast<const f4 *>(arow + kk + h);
     const f4 b = *reinterpret_cast<const f4 *>(brow + kk + h);
 #pragma unroll
