@@ -192,7 +192,7 @@ def main():
                     help="only run a plain device copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the decoder runs on one GPU; --gpus {args.gpus} is not supported "
               "(inputs are independent: shard them over GPUs, one decoder per GPU)", file=sys.stderr)
         sys.exit(2)
 

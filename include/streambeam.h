@@ -43,7 +43,7 @@ typedef enum {
   SB_E_QUEUE_FULL = 4,    /* submit would exceed params.max_inputs                */
   SB_E_TRUNCATED = 5,     /* collect buffers full; the rest stays pending        */
   SB_E_HIP = 6,           /* a HIP runtime call failed (text in sb_last_error)   */
-  SB_E_UNSUPPORTED = 7    /* shape or option this build does not implement       */
+  SB_E_UNSUPPORTED = 7    /* shape or option the library does not implement      */
 } sb_status;
 
 /* Schedulers of Sec. 3 / Alg. 1. Fixed = fixed-width search with the
