@@ -608,7 +608,9 @@ sb_status sb_set_timing(sb_decoder *dec, int32_t enable) {
   if (!dec) return SB_E_INVALID_ARG;
   if (enable && dec->tev.empty()) {
     dec->tev.resize(2 * 1024, nullptr);
-    for (auto &e : dec->tev) HIPCHK(hipEventCreate(&e));
+    // Timing only: no system-scope fences (nothing the host reads depends
+    // on them; the done-flag poll keeps its own fenced events).
+    for (auto &e : dec->tev) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
   }
   dec->timing = enable != 0;
   dec->tev_used = 0;
