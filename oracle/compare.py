@@ -2,11 +2,13 @@
 
 Per input: the token sequences, statuses and the order of the finalized
 hypotheses Y[i] must be identical, and every score must agree with the
-oracle's within `score_tol`. A mismatching input is excused only when the
-oracle logged a decision margin (score gap between two ranked candidates, or
-between a candidate and the relative-threshold boundary) below `tie_tol` at
-some step of that input: such a decision can legitimately go either way under
-rounding, and everything after it may differ.
+oracle's within `score_tol`. An input whose hypotheses differ is excused only
+when the oracle logged a decision margin (score gap between two ranked
+candidates, or between a candidate and the relative-threshold boundary) below
+`tie_tol` at some step of that input: such a decision can legitimately go
+either way under rounding, and everything after it may differ. A score error
+on identical hypotheses is never excused: a near tie changes which tokens are
+kept, not the score of a given token path.
 """
 from __future__ import annotations
 
@@ -56,10 +58,6 @@ def compare(oracle_hyps: Sequence, oracle_min_margin: Sequence[float],
             rep.max_score_err = max(rep.max_score_err, err)
             if err <= score_tol:
                 rep.n_exact += 1
-                continue
-            if tie:
-                rep.n_excused += 1
-                rep.excused.append(i)
                 continue
             rep.failures.append(f"input {i}: score error {err:.3g} > {score_tol}")
             continue

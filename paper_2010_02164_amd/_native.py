@@ -9,6 +9,7 @@ from __future__ import annotations
 import ctypes
 import os
 import re
+import numpy as np
 from ctypes import POINTER, c_char_p, c_double, c_int32, c_int64, c_size_t, c_uint16, c_void_p
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -41,6 +42,13 @@ class SbModel(ctypes.Structure):
 class SbHyp(ctypes.Structure):
     _fields_ = [("input", c_int64), ("rank", c_int32), ("length", c_int32), ("status", c_int32),
                 ("finalize_step", c_int32), ("score", c_double), ("tok_offset", c_int64)]
+
+
+# The same record as a numpy structured type (collect results as arrays).
+SB_HYP_DTYPE = np.dtype({"names": [f for f, _ in SbHyp._fields_],
+                         "formats": [np.int64, np.int32, np.int32, np.int32, np.int32, np.float64, np.int64],
+                         "offsets": [getattr(SbHyp, f).offset for f, _ in SbHyp._fields_],
+                         "itemsize": ctypes.sizeof(SbHyp)})
 
 
 class SbStats(ctypes.Structure):

@@ -49,7 +49,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, kvs, anc, wkvT, xbuf, attn_part, wout_t, total;
+      o_count, o_hyp, o_tok, o_pack, o_off, kvs, anc, wkvT, xbuf, attn_part, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -112,6 +112,8 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.o_count = take(Q * 4);
   L.o_hyp = take(Q * k * sizeof(OutHyp));
   L.o_tok = take(Q * k * MLC * 4);
+  L.o_pack = take(Q * k * MLC * 4);
+  L.o_off = take(Q * k * 8);
   L.wout_t = take(S * 128 * d * es);
   if (m.kv_layers > 0) {
     const size_t planes = (size_t)m.kv_layers * 2;
@@ -341,6 +343,8 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   st.o_count = reinterpret_cast<int32_t *>(w + L.o_count);
   st.o_hyp = reinterpret_cast<OutHyp *>(w + L.o_hyp);
   st.o_tok = reinterpret_cast<int32_t *>(w + L.o_tok);
+  st.o_pack = reinterpret_cast<int32_t *>(w + L.o_pack);
+  st.o_off = reinterpret_cast<int64_t *>(w + L.o_off);
   if (model->kv_layers > 0) {
     st.kvs = reinterpret_cast<uint16_t *>(w + L.kvs);
     st.anc = reinterpret_cast<uint8_t *>(w + L.anc);
@@ -548,11 +552,9 @@ sb_status sb_collect(sb_decoder *dec, sb_hyp *hyps, int64_t hyp_cap, int32_t *to
     q_end = q + 1;
   }
   if (q_end > q0) {
-    const size_t rows = (size_t)(q_end - q0) * k;
-    std::vector<int32_t> tk(rows * MLC);
-    HIPCHK(hipMemcpyAsync(tk.data(), dec->st.o_tok + (size_t)q0 * k * MLC, sizeof(int32_t) * rows * MLC,
-                          hipMemcpyDeviceToHost, dec->stream));
-    HIPCHK(hipStreamSynchronize(dec->stream));
+    // Records on the host; the tokens are packed on the device in the same
+    // order and copied in one piece (only the tokens the hypotheses hold).
+    std::vector<int64_t> off((size_t)(q_end - q0) * k, -1);
     int64_t h = 0, t = 0;
     for (int q = q0; q < q_end; ++q) {
       const int c = cnt[q - q0];
@@ -566,10 +568,16 @@ sb_status sb_collect(sb_decoder *dec, sb_hyp *hyps, int64_t hyp_cap, int32_t *to
         y.finalize_step = o.finalize_step;
         y.score = o.score;
         y.tok_offset = t;
-        memcpy(tokens + t, tk.data() + ((size_t)(q - q0) * k + r) * MLC, sizeof(int32_t) * o.length);
+        off[(size_t)(q - q0) * k + r] = t;
         t += o.length;
       }
     }
+    HIPCHK(hipMemcpyAsync(dec->st.o_off, off.data(), sizeof(int64_t) * off.size(), hipMemcpyHostToDevice,
+                          dec->stream));
+    HIPCHK(launch_pack(dec->st, q0, q_end, dec->stream));
+    if (t > 0)
+      HIPCHK(hipMemcpyAsync(tokens, dec->st.o_pack, sizeof(int32_t) * t, hipMemcpyDeviceToHost, dec->stream));
+    HIPCHK(hipStreamSynchronize(dec->stream));
   }
   *n_hyps = nh;
   *n_tokens = nt;

@@ -659,6 +659,22 @@ __global__ __launch_bounds__(256) void k_backtrack(DevState st, int q0, int q1) 
   h->length = len;
 }
 
+// Collect: copy the tokens of the hypotheses of inputs [q0, q1) from their
+// padded rows to their places in the packed buffer (offsets set by the
+// host; -1 marks a rank the input does not have). Four hypotheses per
+// workgroup, one wave each, lanes striding over the tokens.
+__global__ __launch_bounds__(256) void k_pack(DevState st, int q0, int q1) {
+  const long long hyp = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (hyp >= (long long)(q1 - q0) * st.k) return;
+  const long long off = st.o_off[hyp];
+  if (off < 0) return;
+  const size_t slot = (size_t)q0 * st.k + hyp;
+  const int len = min(st.o_hyp[slot].length, st.max_len_cap);
+  const int32_t *src = st.o_tok + slot * st.max_len_cap;
+  for (int j = lane; j < len; j += 64) st.o_pack[off + j] = src[j];
+}
+
 }  // namespace
 
 hipError_t launch_rowmerge(const DevState &st, hipStream_t s) {
@@ -698,6 +714,13 @@ hipError_t launch_beam(const DevState &st, hipStream_t s) {
       break;
   }
 #undef SB_BEAM
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const DevState &st, int q0, int q1, hipStream_t s) {
+  if (q1 <= q0) return hipSuccess;
+  const long long hyps = (long long)(q1 - q0) * st.k;
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)((hyps + 3) / 4)), dim3(256), 0, s, st, q0, q1);
   return hipGetLastError();
 }
 

@@ -76,6 +76,8 @@ struct DevState {
   int32_t *o_count;    // [max_inputs] |Y[i]| (0 = unfinished)
   OutHyp *o_hyp;       // [max_inputs][k]
   int32_t *o_tok;      // [max_inputs][k][max_len_cap]
+  int32_t *o_pack;     // [max_inputs * k * max_len_cap] collected tokens, packed back to back
+  int64_t *o_off;      // [max_inputs][k] offset of each collected hypothesis in o_pack (-1: none)
   // KV-like state (bf16 bits). The row produced by expanding the candidate
   // at (beam, level, rank) is stored once, at kvs[beam][level][rank]; a
   // candidate's rows are those of its ancestors, whose ranks per level it
@@ -125,6 +127,7 @@ hipError_t launch_beam(const DevState &st, hipStream_t s);
 hipError_t launch_kv_append(const DevState &st, hipStream_t s);
 hipError_t launch_attn(const DevState &st, hipStream_t s);
 hipError_t launch_backtrack(const DevState &st, int q0, int q1, hipStream_t s);
+hipError_t launch_pack(const DevState &st, int q0, int q1, hipStream_t s);
 hipError_t launch_init(const DevState &st, hipStream_t s);
 hipError_t launch_relayout_wout(const DevState &st, hipStream_t s);
 hipError_t launch_transpose_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s);

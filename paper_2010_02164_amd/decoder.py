@@ -159,27 +159,46 @@ class Decoder:
     def run(self):
         _check(N.lib().sb_run(self.handle), "sb_run", self.handle)
 
-    def collect(self) -> List[Hypothesis]:
+    def collect_arrays(self) -> dict:
+        """Finalized hypotheses not yet collected, as numpy arrays (no
+        per-hypothesis Python objects): `input`, `rank`, `length`, `status`,
+        `finalize_step`, `score`, `tok_offset` (one entry per hypothesis, in
+        input then rank order) and `tokens` (all token ids back to back;
+        hypothesis j holds tokens[tok_offset[j] : tok_offset[j] + length[j]])."""
         L = N.lib()
-        out: List[Hypothesis] = []
         cap_h = max(16, self.n_submitted * self.k)
         cap_t = max(64, cap_h * int(self.params.max_len_cap))
-        hyps = (N.SbHyp * cap_h)()
-        toks = np.empty(cap_t, dtype=np.int32)
+        recs, toks = [], []
+        base = 0
         while True:
+            hyps = np.empty(cap_h, dtype=N.SB_HYP_DTYPE)
+            tk = np.empty(cap_t, dtype=np.int32)
             nh, nt = ctypes.c_int64(0), ctypes.c_int64(0)
-            st = L.sb_collect(self.handle, hyps, cap_h, toks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                              cap_t, ctypes.byref(nh), ctypes.byref(nt))
+            st = L.sb_collect(self.handle, hyps.ctypes.data_as(ctypes.POINTER(N.SbHyp)), cap_h,
+                              tk.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cap_t, ctypes.byref(nh),
+                              ctypes.byref(nt))
             if st not in (N.SB_OK, N.SB_E_TRUNCATED):
                 _check(st, "sb_collect", self.handle)
-            for i in range(nh.value):
-                h = hyps[i]
-                out.append(Hypothesis(int(h.input), int(h.rank),
-                                      tuple(int(x) for x in toks[h.tok_offset:h.tok_offset + h.length]),
-                                      float(h.score), int(h.status), int(h.finalize_step)))
+            h = hyps[:nh.value].copy() if st == N.SB_E_TRUNCATED else hyps[:nh.value]
+            h["tok_offset"] += base
+            recs.append(h)
+            toks.append(tk[:nt.value])
+            base += nt.value
             if st == N.SB_OK or nh.value == 0:
                 break
+        h = recs[0] if len(recs) == 1 else np.concatenate(recs)
+        out = {f: h[f] for f in h.dtype.names}
+        out["tokens"] = toks[0] if len(toks) == 1 else np.concatenate(toks)
         return out
+
+    def collect(self) -> List[Hypothesis]:
+        """Finalized hypotheses not yet collected, as Hypothesis objects."""
+        a = self.collect_arrays()
+        tokens = a["tokens"].tolist()
+        return [Hypothesis(int(i), int(r), tuple(tokens[o:o + n]), float(sc), int(st), int(f))
+                for i, r, n, st, f, sc, o in zip(a["input"].tolist(), a["rank"].tolist(), a["length"].tolist(),
+                                                 a["status"].tolist(), a["finalize_step"].tolist(),
+                                                 a["score"].tolist(), a["tok_offset"].tolist())]
 
     def stats(self) -> dict:
         s = N.SbStats()

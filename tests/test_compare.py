@@ -30,3 +30,11 @@ def test_near_tie_excuses_mismatch():
     g = [[((1, 3, 0), -1.0, 2)]]
     r = compare(O, [5e-5], g, inputs=[7])
     assert r.ok and r.n_excused == 1 and r.excused == [7]
+
+
+def test_score_error_on_identical_outputs_is_never_excused():
+    # Same tokens, statuses and order, but a score off by more than the
+    # tolerance: a near tie cannot explain it, whatever the logged margin.
+    g = [[((1, 2, 0), -1.01, 2), ((1, 0), -1.5, 2)]]
+    r = compare(O, [1e-9], g)
+    assert not r.ok and r.n_excused == 0

@@ -70,3 +70,4 @@ def test_cfg6_full_size_sampled(gpu):
                   score_tol=score_tol(wl), tie_tol=tie_tol(wl))
     print(f"[parity] cfg6 full, sampled: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures
+    assert rep.n_excused == 0, rep.excused

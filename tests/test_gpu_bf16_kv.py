@@ -7,7 +7,7 @@ import pytest
 from oracle.decoder import ElmanDecoder
 from synthgen import make_workload, scaled
 from synthgen.gen import bf16_bits_to_f32, f32_to_bf16_bits
-from tests.gpu_util import check_parity, gpu_decode
+from tests.gpu_util import check_parity, gpu_decode, length_sample, sampled_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -15,16 +15,34 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("sched,eps", [("var_batch", None), ("var_stream", 0.125), ("var_stream", 0.5),
                                        ("fixed", None), ("var_fifo", 0.25)])
 def test_cfg4_reduced(gpu, sched, eps):
-    wl = make_workload(scaled(4, N=48, n=16, V=8000))
+    # |V| = 8320 (65 tiles): the short tile lists of the full vocabulary.
+    wl = make_workload(scaled(4, N=48, n=16, V=8320))
     rep, _, _, _ = check_parity(wl, sched, eps=eps)
     # bf16 states are reproduced exactly, so scores match like fp32 ones
     assert rep.max_score_err < 1e-4
 
 
-@pytest.mark.parametrize("sched", ["var_stream", "var_fifo"])
+@pytest.mark.parametrize("sched", ["fixed", "var_batch", "var_stream", "var_fifo"])
 def test_cfg5_reduced_search(gpu, sched):
-    wl = make_workload(scaled(5, N=24, n=8, V=6000, len_hi=30))
+    wl = make_workload(scaled(5, N=24, n=8, V=8320, len_hi=30))
     check_parity(wl, sched)
+
+
+@pytest.mark.parametrize("sched,eps", [("var_stream", None), ("var_batch", None), ("fixed", None),
+                                       ("var_stream", 0.125)])
+def test_cfg4_full_size_sampled(gpu, sched, eps):
+    # The full bf16 wide-beam workload: 8192 inputs, n = 512, k = 10 (steps
+    # of up to 5 120 rows), |V| = 32000, d = 1024; 48 inputs over the length
+    # distribution (the 8 longest included) decoded by the oracle as one
+    # batch.
+    from synthgen import get_config
+    wl = make_workload(get_config(4))
+    g, st, dec = gpu_decode(wl, sched, eps=eps)
+    counts, width = dec.rows_histogram()
+    dec.close()
+    assert st["finished"] == len(wl.Lx) and st["hyps"] == sum(len(y) for y in g)
+    assert sum(c for i, c in enumerate(counts) if i * width >= 4096) > 0   # full-size steps ran
+    sampled_parity(wl, g, length_sample(wl, 48), f"cfg4 full {sched} eps={eps}, 48 sampled", sched)
 
 
 def _kv_reference(wl, dec_o, i, tokens):

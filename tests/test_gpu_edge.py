@@ -115,6 +115,7 @@ def test_largest_rows_and_state(gpu):
     rep = compare(hy, mm, [[(h.tokens, h.score, h.status) for h in g[i]] for i in sample], inputs=sample)
     print(f"[parity] n=4096 k=16 d=4096 sampled: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures
+    assert rep.n_excused == 0, rep.excused
 
 
 def test_long_outputs(gpu):
@@ -148,7 +149,6 @@ def test_exact_ties_follow_rank_key(gpu, cfg_i, over, pairs, sched, kw):
     # recomputed and every logit comes from the projection kernel.
     wl = make_workload(scaled(cfg_i, **over))
     _plant_ties(wl, pairs)
-    rep, g, st, o = check_parity(wl, sched, **kw)
+    rep, g, st, o = check_parity(wl, sched, max_excused=len(wl.Lx) // 3, **kw)
     tied = sum(1 for y in o.hyps for i in range(len(y)) for j in range(i + 1, len(y)) if y[i].score == y[j].score)
     assert tied > 0                                  # the ties reach the outputs
-    assert rep.n_excused <= rep.n_inputs // 3        # most inputs compared strictly

@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 from synthgen import get_config, make_workload, scaled
-from tests.gpu_util import check_parity, gpu_decode
+from tests.gpu_util import check_parity, gpu_decode, length_sample, sampled_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -25,9 +25,13 @@ def test_cfg2_reduced(gpu, sched):
     check_parity(wl, sched)
 
 
-@pytest.mark.parametrize("sched", ["var_batch", "var_stream", "var_fifo", "fixed_fairseq_stream", "var_cap"])
+@pytest.mark.parametrize("sched", ["fixed", "fixed_stream", "var_batch", "var_stream", "var_fifo",
+                                   "fixed_fairseq_stream", "var_cap"])
 def test_cfg3_reduced(gpu, sched):
-    wl = make_workload(scaled(3, N=40, n=16, V=8000))
+    # |V| = 8320: 65 tiles of 128 tokens, so the projection keeps the short
+    # 4-key tile lists and the row merge runs its completion check, as on
+    # the full 32 000-token vocabulary.
+    wl = make_workload(scaled(3, N=40, n=16, V=8320))
     check_parity(wl, sched)
 
 
@@ -109,26 +113,28 @@ def test_deterministic(gpu):
         assert [(h.tokens, h.score) for h in ya] == [(h.tokens, h.score) for h in yb]
 
 
-def test_cfg3_full_size_sampled(gpu):
-    # The full MT-shaped fp32 workload (4096 inputs, |V| = 32000) in the
-    # configuration the benchmark runs; a sample of inputs is decoded by the
-    # oracle one at a time (results are per input, Sec. 3).
-    from oracle.compare import compare
-    from oracle.search import decode_workload
-    from synthgen import get_config
+@pytest.mark.parametrize("sched", ["var_stream", "var_batch"])
+def test_cfg3_full_size_sampled(gpu, sched):
+    # The full MT-shaped fp32 workload (4096 inputs, n = 128, |V| = 32000)
+    # in the configuration the benchmark runs; 64 inputs spread over the
+    # length distribution (the 8 longest included) are decoded by the
+    # oracle as one batch (results are per input, Sec. 3).
     wl = make_workload(get_config(3))
-    g, st, dec = gpu_decode(wl, "var_stream")
+    g, st, dec = gpu_decode(wl, sched)
     dec.close()
     assert st["finished"] == len(wl.Lx) and st["hyps"] == sum(len(y) for y in g)
-    sample = [0, 1, 777, 2048, 4095]
-    hy, mm = [], []
-    for i in sample:
-        o = decode_workload(wl, inputs=[i])
-        hy.append(o.hyps[0])
-        mm.append(o.min_margin[0])
-    rep = compare(hy, mm, [[(h.tokens, h.score, h.status) for h in g[i]] for i in sample], inputs=sample)
-    print(f"[parity] cfg3 full, sampled: {rep.summary()}", flush=True)
-    assert rep.ok, rep.failures
+    sampled_parity(wl, g, length_sample(wl, 64), f"cfg3 full {sched}, 64 sampled", sched)
+
+
+@pytest.mark.parametrize("sched", ["var_stream", "var_batch", "fixed"])
+def test_cfg2_full_size_sampled(gpu, sched):
+    # The full parsing-shaped workload: 16 384 inputs, n = 1024, k = 5
+    # (steps of up to 5 120 rows), |V| = 256, d = 256; 256 sampled inputs.
+    wl = make_workload(get_config(2))
+    g, st, dec = gpu_decode(wl, sched)
+    dec.close()
+    assert st["finished"] == len(wl.Lx) and st["hyps"] == sum(len(y) for y in g)
+    sampled_parity(wl, g, length_sample(wl, 256, longest=16), f"cfg2 full {sched}, 256 sampled", sched)
 
 
 def _clustered(cfg, seed=5):

@@ -16,6 +16,7 @@ import oracle.decoder
 import oracle.search
 import tests.test_oracle_attention as tattn
 import tests.test_oracle_decoder as tdec
+import tests.test_oracle_margins as tmargin
 import tests.test_oracle_search as tsearch
 
 
@@ -56,6 +57,14 @@ PINS = {
     "attn_uniform": lambda: tattn.test_uniform_scores_average_the_value_rows(0),
     "attn_two": lambda: tattn.test_two_positions_logistic_form(1),
     "attn_recurrence": tattn.test_recurrence_reads_h_not_the_attention_input,
+    "margin_kth": tmargin.test_margin_kth_versus_next,
+    "margin_adjacent": tmargin.test_margin_adjacent_ranks,
+    "margin_noop": tmargin.test_margin_with_noop_and_two_parents,
+    "margin_delta": tmargin.test_margin_threshold_boundary,
+    "margin_delta_pruned": tmargin.test_margin_threshold_boundary_of_a_pruned_member,
+    "margin_tie": tmargin.test_exact_tie_is_no_margin,
+    "margin_fairseq": tmargin.test_fairseq_margin_window,
+    "margin_search": tmargin.test_search_keeps_the_smallest_margin_of_an_input,
 }
 
 MUTATIONS = [
@@ -93,6 +102,25 @@ MUTATIONS = [
      ["attn_recurrence"]),
     ("attn_input_not_rounded", "decoder", "x[r] = bf16_round(h[r] + self.attention(h[r], K, V))",
      "x[r] = h[r] + self.attention(h[r], K, V)", ["attn_single"]),
+    ("margin_only_kth_cut", "beam", "for a, b in zip(pool[:k], pool[1:k + 1]):",
+     "for a, b in zip(pool[k - 1:k], pool[k:k + 1]):", ["margin_adjacent"]),
+    ("margin_misses_kth_cut", "beam", "for a, b in zip(pool[:k], pool[1:k + 1]):",
+     "for a, b in zip(pool[:k - 1], pool[1:k]):", ["margin_kth", "margin_noop"]),
+    ("margin_counts_exact_ties", "beam", "for a, b in zip(pool[:k], pool[1:k + 1]):\n        if a[0] != b[0]:",
+     "for a, b in zip(pool[:k], pool[1:k + 1]):\n        if True:", ["margin_tie"]),
+    ("margin_drops_threshold_boundary", "beam", "margin = min(margin, abs(score - (ref - delta)))", "pass",
+     ["margin_delta", "margin_delta_pruned"]),
+    ("margin_skips_pruned_members", "beam",
+     "            margin = min(margin, abs(score - (ref - delta)))\n            if score < ref - delta:\n"
+     "                continue\n",
+     "            if score < ref - delta:\n                continue\n"
+     "            margin = min(margin, abs(score - (ref - delta)))\n", ["margin_delta_pruned"]),
+    ("margin_boundary_without_abs", "beam", "margin = min(margin, abs(score - (ref - delta)))",
+     "margin = min(margin, (ref - delta) - score)", ["margin_delta"]),
+    ("fairseq_margin_window_short", "beam", "head = pool[:2 * k + 1]", "head = pool[:k + 1]", ["margin_fairseq"]),
+    ("min_margin_keeps_last_step", "search",
+     "res.min_margin[b.input] = min(res.min_margin[b.input], margin)", "res.min_margin[b.input] = margin",
+     ["margin_search"]),
     ("refill_strict", "search", "len(live) <= eps * P", "len(live) < eps * P", ["fig1", "cap_schedule"]),
     ("refill_against_n", "search", "len(live) <= eps * P", "len(live) <= eps * n", ["cap_schedule"]),
     ("refill_to_n", "search", "m = min(P - len(live), N - c)", "m = min(n - len(live), N - c)",
@@ -120,11 +148,13 @@ def test_planted_mistake_is_caught(monkeypatch, name, modname, old, new, pins):
                 if hasattr(target, attr):
                     monkeypatch.setattr(target, attr, getattr(mut, attr))
     elif modname == "beam":
-        monkeypatch.setattr(oracle.search, "beam_step", mut.beam_step)
-        monkeypatch.setattr(oracle.search, "beam_step_fairseq", mut.beam_step_fairseq)
+        for target in (oracle.search, tmargin):
+            monkeypatch.setattr(target, "beam_step", mut.beam_step)
+            monkeypatch.setattr(target, "beam_step_fairseq", mut.beam_step_fairseq)
     else:
         for attr in ("decode", "decode_workload"):
             monkeypatch.setattr(tsearch, attr, getattr(mut, attr))
+        monkeypatch.setattr(tmargin, "decode", mut.decode)
     for pin in pins:
         with pytest.raises(Exception):
             PINS[pin]()
