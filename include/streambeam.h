@@ -19,7 +19,9 @@
  *  - The caller owns all device memory (weights, the workspace, h0 staging);
  *    it must outlive the decoder. The library never allocates or frees device
  *    memory; it owns a small host-side object, pinned host staging for the
- *    per-input lengths (8 bytes per queue entry) and a few HIP events.
+ *    per-input lengths (8 bytes per queue entry) and a few HIP events. The
+ *    one exception is sb_create_noalloc, whose decoders use a static device
+ *    array of the library in place of a caller workspace.
  *  - All device work is ordered on the decoder's stream.
  *  - No call aborts or throws across the ABI. Errors return an sb_status;
  *    sb_last_error() gives the text of the decoder's last failure.
@@ -174,6 +176,29 @@ sb_status sb_validate(const sb_model *model, const sb_params *params);
 sb_status sb_create(const sb_model *model, const sb_params *params, void *workspace,
                     size_t bytes, void *stream, sb_decoder **out);
 
+/* Largest workspace (bytes) a decoder made by sb_create_noalloc can use. */
+#define SB_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): sb_create
+ * without a caller workspace. The decoder uses the library's static scratch,
+ * a device array of SB_NOALLOC_SCRATCH_BYTES that each GPU the library runs
+ * on holds until the process ends, and static host storage for the decoder
+ * object; the call makes no device or pinned-host allocation (no hipMalloc,
+ * hipHostMalloc, hipFree, event or stream creation).
+ *  - Shapes whose workspace (sb_workspace_bytes) exceeds the scratch return
+ *    SB_E_WORKSPACE; sb_last_error(NULL) gives the sizes.
+ *  - One such decoder per GPU at a time: while one is alive (until
+ *    sb_destroy), another call on the same GPU returns SB_E_STATE. The
+ *    scratch keeps the last decoder's contents; sb_create_noalloc
+ *    initialises everything the search reads.
+ *  - Otherwise the decoder behaves as one from sb_create, with two
+ *    differences: sb_submit waits for its length copies before returning
+ *    (there is no pinned staging), and the first sb_run creates the two
+ *    events it polls with.
+ * The weights are read, never written, and must outlive the decoder. */
+sb_status sb_create_noalloc(const sb_model *model, const sb_params *params, void *stream, sb_decoder **out);
+
 /* Append `count` inputs to the queue (Alg. 1's X, in index order).
  * ids: host [count] caller ids echoed in sb_hyp.input, or NULL for the
  * queue positions. h0: device [count][d] (dtype of the model), the
@@ -246,6 +271,8 @@ sb_status sb_debug_slot(sb_decoder *dec, int32_t beam, int32_t rank, int32_t *st
                         int32_t tok_cap, int32_t *n_tokens, uint16_t *kv, int64_t kv_cap);
 
 sb_status sb_destroy(sb_decoder *dec);
+/* Text of the decoder's last failure; with dec == NULL, of the calling
+ * thread's last failed sb_create_noalloc. */
 const char *sb_last_error(const sb_decoder *dec);
 const char *sb_status_string(sb_status s);
 

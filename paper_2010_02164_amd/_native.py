@@ -16,6 +16,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libstreambeam.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "streambeam.h")
 
+# Workspace limit of sb_create_noalloc (SB_NOALLOC_SCRATCH_BYTES in the header).
+SB_NOALLOC_SCRATCH_BYTES = 64 << 20
+
 SB_OK, SB_E_INVALID_ARG, SB_E_WORKSPACE, SB_E_STATE, SB_E_QUEUE_FULL, SB_E_TRUNCATED, \
     SB_E_HIP, SB_E_UNSUPPORTED = range(8)
 SB_FIXED, SB_VAR_BATCH, SB_VAR_STREAM, SB_VAR_FIFO, SB_FIXED_STREAM, SB_VAR_CAP = 0, 1, 2, 3, 4, 5
@@ -87,6 +90,7 @@ def lib():
         "sb_workspace_bytes": (c_size_t, [P(SbModel), P(SbParams)]),
         "sb_validate": (c_int32, [P(SbModel), P(SbParams)]),
         "sb_create": (c_int32, [P(SbModel), P(SbParams), c_void_p, c_size_t, c_void_p, P(c_void_p)]),
+        "sb_create_noalloc": (c_int32, [P(SbModel), P(SbParams), c_void_p, P(c_void_p)]),
         "sb_submit": (c_int32, [c_void_p, c_int32, P(c_int64), c_void_p, P(c_int32), P(c_int32)]),
         "sb_step": (c_int32, [c_void_p, P(c_int32)]),
         "sb_run": (c_int32, [c_void_p]),

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -24,8 +25,11 @@ struct sb_decoder {
   size_t ws_bytes;
   int32_t n_queued = 0;
   int32_t collected = 0;       // inputs already returned by sb_collect
-  int32_t *pinned_len = nullptr;   // [2][max_inputs] L_x and max_len staging
-  int32_t *pinned_flag = nullptr;  // [2] done-flag readback
+  int32_t *pinned_len = nullptr;   // [2][max_inputs] L_x and max_len staging (none: noalloc)
+  int32_t *pinned_flag = nullptr;  // [2] done-flag readback (noalloc: host_flag below)
+  int32_t host_flag[2] = {0, 0};   // done-flag readback of a decoder that allocates nothing
+  int device = 0;
+  bool noalloc = false;            // lives in the library's static storage (sb_create_noalloc)
   hipEvent_t poll_ev[2] = {nullptr, nullptr};
   bool timing = false;
   double proj_ms = 0.0;
@@ -268,6 +272,34 @@ sb_status launch_timed_step(sb_decoder *dec) {
 
 }  // namespace
 
+// Workspace of the allocation-free decoders (below).
+static __device__ __align__(256) unsigned char scratch[SB_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Allocation-free decoders (sb_create_noalloc). The workspace is a static
+// device array, one copy per GPU the library runs on, held until the process
+// ends; the decoder object is static host storage, one per GPU. In host code
+// `scratch` names a host-side stand-in: kernels and copies get the device
+// address that hipGetSymbolAddress returns for the current device.
+constexpr int NOALLOC_MAX_DEVICES = 64;
+
+struct NoallocSlot {
+  unsigned char *ptr = nullptr;   // device address of `scratch` on this GPU
+  bool in_use = false;            // a noalloc decoder on this GPU is alive
+  alignas(sb_decoder) unsigned char obj[sizeof(sb_decoder)];
+};
+NoallocSlot g_noalloc[NOALLOC_MAX_DEVICES];
+std::mutex g_noalloc_mu;
+thread_local char g_create_err[256] = "";
+
+void set_create_err(const char *msg) {
+  snprintf(g_create_err, sizeof g_create_err, "%s", msg);
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *sb_status_string(sb_status s) {
@@ -293,19 +325,21 @@ size_t sb_workspace_bytes(const sb_model *model, const sb_params *params) {
   return layout_of(*model, *params).total;
 }
 
-const char *sb_last_error(const sb_decoder *dec) { return dec ? dec->err.c_str() : "null decoder"; }
+const char *sb_last_error(const sb_decoder *dec) {
+  if (dec) return dec->err.c_str();
+  return g_create_err[0] ? g_create_err : "null decoder";
+}
 
-sb_status sb_create(const sb_model *model, const sb_params *params, void *workspace, size_t bytes,
-                    void *stream, sb_decoder **out) {
-  if (!out) return SB_E_INVALID_ARG;
-  *out = nullptr;
-  sb_status s = check(model, params, nullptr);
-  if (s != SB_OK) return s;
-  if (!model->W_h || !model->E || !model->W_out) return SB_E_INVALID_ARG;
+}  // extern "C"
+
+namespace {
+
+// Set up `dec` over `workspace` (already checked to hold the layout) and
+// initialise the device state on `stream`. On failure the caller disposes of
+// the decoder with sb_destroy.
+sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *params, void *workspace,
+                       size_t bytes, void *stream) {
   const Layout L = layout_of(*model, *params);
-  if (!workspace || ((uintptr_t)workspace % ALIGN) != 0 || bytes < L.total) return SB_E_WORKSPACE;
-  sb_decoder *dec = new (std::nothrow) sb_decoder();
-  if (!dec) return SB_E_INVALID_ARG;
   dec->model = *model;
   dec->params = effective(*params);
   dec->stream = static_cast<hipStream_t>(stream);
@@ -383,32 +417,119 @@ sb_status sb_create(const sb_model *model, const sb_params *params, void *worksp
   {
     int dev = 0, ncu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0) {
-      sb_destroy(dec);
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
       return SB_E_HIP;
-    }
     st.n_cu = ncu;
+    dec->device = dev;
   }
   st.delta = p.delta;
   st.beta = model->eos_beta;
 
-  auto fail = [&](sb_status code) {
-    sb_destroy(dec);
-    return code;
-  };
-  if (hipHostMalloc(reinterpret_cast<void **>(&dec->pinned_len), sizeof(int32_t) * 2 * (size_t)p.max_inputs,
-                    hipHostMallocDefault) != hipSuccess)
-    return fail(SB_E_HIP);
-  if (hipHostMalloc(reinterpret_cast<void **>(&dec->pinned_flag), sizeof(int32_t) * 2, hipHostMallocDefault) !=
-      hipSuccess)
-    return fail(SB_E_HIP);
-  for (int i = 0; i < 2; ++i)
-    if (hipEventCreateWithFlags(&dec->poll_ev[i], hipEventDisableTiming) != hipSuccess) return fail(SB_E_HIP);
-  if (launch_init(st, dec->stream) != hipSuccess) return fail(SB_E_HIP);
-  if (launch_relayout_wout(st, dec->stream) != hipSuccess) return fail(SB_E_HIP);
+  if (dec->noalloc) {
+    // No pinned staging: submits copy straight from the caller's arrays
+    // and wait; the done flag is read back into the decoder object. The
+    // poll events are made by the first sb_run.
+    dec->pinned_flag = dec->host_flag;
+  } else {
+    if (hipHostMalloc(reinterpret_cast<void **>(&dec->pinned_len), sizeof(int32_t) * 2 * (size_t)p.max_inputs,
+                      hipHostMallocDefault) != hipSuccess)
+      return SB_E_HIP;
+    if (hipHostMalloc(reinterpret_cast<void **>(&dec->pinned_flag), sizeof(int32_t) * 2, hipHostMallocDefault) !=
+        hipSuccess)
+      return SB_E_HIP;
+    for (int i = 0; i < 2; ++i)
+      if (hipEventCreateWithFlags(&dec->poll_ev[i], hipEventDisableTiming) != hipSuccess) return SB_E_HIP;
+  }
+  if (launch_init(st, dec->stream) != hipSuccess) return SB_E_HIP;
+  if (launch_relayout_wout(st, dec->stream) != hipSuccess) return SB_E_HIP;
   if (model->kv_layers > 0 &&
       launch_transpose_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
-    return fail(SB_E_HIP);
+    return SB_E_HIP;
+  return SB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sb_status sb_create(const sb_model *model, const sb_params *params, void *workspace, size_t bytes,
+                    void *stream, sb_decoder **out) {
+  if (!out) return SB_E_INVALID_ARG;
+  *out = nullptr;
+  sb_status s = check(model, params, nullptr);
+  if (s != SB_OK) return s;
+  if (!model->W_h || !model->E || !model->W_out) return SB_E_INVALID_ARG;
+  const Layout L = layout_of(*model, *params);
+  if (!workspace || ((uintptr_t)workspace % ALIGN) != 0 || bytes < L.total) return SB_E_WORKSPACE;
+  sb_decoder *dec = new (std::nothrow) sb_decoder();
+  if (!dec) return SB_E_INVALID_ARG;
+  s = init_decoder(dec, model, params, workspace, bytes, stream);
+  if (s != SB_OK) {
+    sb_destroy(dec);
+    return s;
+  }
+  *out = dec;
+  return SB_OK;
+}
+
+sb_status sb_create_noalloc(const sb_model *model, const sb_params *params, void *stream, sb_decoder **out) {
+  if (!out) return SB_E_INVALID_ARG;
+  *out = nullptr;
+  std::string why;
+  sb_status s = check(model, params, &why);
+  if (s != SB_OK) {
+    set_create_err(why.c_str());
+    return s;
+  }
+  if (!model->W_h || !model->E || !model->W_out) {
+    set_create_err("sb_create_noalloc: null weight pointer");
+    return SB_E_INVALID_ARG;
+  }
+  const size_t need = layout_of(*model, *params).total;
+  if (need > SB_NOALLOC_SCRATCH_BYTES) {
+    char msg[256];
+    snprintf(msg, sizeof msg,
+             "sb_create_noalloc: these shapes need %zu bytes of workspace; the static scratch holds %zu "
+             "(use sb_create with a caller workspace)",
+             need, (size_t)SB_NOALLOC_SCRATCH_BYTES);
+    set_create_err(msg);
+    return SB_E_WORKSPACE;
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= NOALLOC_MAX_DEVICES) {
+    set_create_err("sb_create_noalloc: no usable current device");
+    return SB_E_HIP;
+  }
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  NoallocSlot &slot = g_noalloc[dev];
+  if (slot.in_use) {
+    set_create_err("sb_create_noalloc: a decoder over this GPU's static scratch is still alive");
+    return SB_E_STATE;
+  }
+  if (!slot.ptr) {
+    // Once per device, with that device current: the device address of
+    // this GPU's copy of the array.
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      char msg[256];
+      snprintf(msg, sizeof msg, "sb_create_noalloc: hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      set_create_err(msg);
+      return SB_E_HIP;
+    }
+    slot.ptr = static_cast<unsigned char *>(p);
+  }
+  sb_decoder *dec = new (slot.obj) sb_decoder();
+  dec->noalloc = true;
+  slot.in_use = true;
+  s = init_decoder(dec, model, params, slot.ptr, SB_NOALLOC_SCRATCH_BYTES, stream);
+  if (s != SB_OK) {
+    set_create_err(dec->err.empty() ? "sb_create_noalloc: HIP call failed" : dec->err.c_str());
+    (void)hipStreamSynchronize(dec->stream);   // nothing enqueued may still write the scratch
+    dec->~sb_decoder();
+    slot.in_use = false;
+    return s;
+  }
   *out = dec;
   return SB_OK;
 }
@@ -447,10 +568,16 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const int64_t *ids, const vo
   for (int i = 0; i < count; ++i) dec->ids[q0 + i] = ids ? ids[i] : (int64_t)(q0 + i);
   const size_t es = dec->model.dtype == SB_BF16 ? 2 : 4;
   const size_t rowbytes = (size_t)dec->model.d * es;
-  int32_t *lx = dec->pinned_len + q0;
-  int32_t *ml = dec->pinned_len + p.max_inputs + q0;
-  memcpy(lx, L_x, sizeof(int32_t) * count);
-  memcpy(ml, max_len, sizeof(int32_t) * count);
+  // Lengths go through the pinned staging; a decoder without it (noalloc)
+  // copies from the caller's arrays and waits below.
+  const int32_t *lx = L_x, *ml = max_len;
+  if (dec->pinned_len) {
+    int32_t *slx = dec->pinned_len + q0, *sml = dec->pinned_len + p.max_inputs + q0;
+    memcpy(slx, L_x, sizeof(int32_t) * count);
+    memcpy(sml, max_len, sizeof(int32_t) * count);
+    lx = slx;
+    ml = sml;
+  }
   HIPCHK(hipMemcpyAsync(static_cast<unsigned char *>(dec->st.q_h0) + q0 * rowbytes, h0, count * rowbytes,
                         hipMemcpyDeviceToDevice, dec->stream));
   HIPCHK(hipMemcpyAsync(dec->st.q_Lx + q0, lx, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
@@ -458,6 +585,7 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const int64_t *ids, const vo
   dec->n_queued += count;
   hipLaunchKernelGGL(k_set_queued, dim3(1), dim3(1), 0, dec->stream, dec->st.ctrl, dec->n_queued);
   HIPCHK(hipGetLastError());
+  if (!dec->pinned_len) HIPCHK(hipStreamSynchronize(dec->stream));
   return SB_OK;
 }
 
@@ -480,6 +608,8 @@ sb_status sb_run(sb_decoder *dec) {
   // takes at most max_len_cap steps, so this bounds any correct run.
   const int64_t limit = ((int64_t)dec->n_queued + pool_of(dec->params)) * (dec->params.max_len_cap + 1) + 64;
   const bool timed = dec->timing;
+  for (int i = 0; i < 2; ++i)   // made here for decoders that allocate nothing at creation
+    if (!dec->poll_ev[i]) HIPCHK(hipEventCreateWithFlags(&dec->poll_ev[i], hipEventDisableTiming));
   if (!timed && !dec->graph_exec) {
     sb_status s = capture(dec, &dec->graph, &dec->graph_exec);
     if (s != SB_OK) return s;
@@ -736,10 +866,18 @@ sb_status sb_destroy(sb_decoder *dec) {
   for (int i = 0; i < 2; ++i)
     if (dec->poll_ev[i]) (void)hipEventDestroy(dec->poll_ev[i]);
   if (dec->pinned_len) (void)hipHostFree(dec->pinned_len);
-  if (dec->pinned_flag) (void)hipHostFree(dec->pinned_flag);
+  if (dec->pinned_flag && dec->pinned_flag != dec->host_flag) (void)hipHostFree(dec->pinned_flag);
   if (dec->graph_exec) (void)hipGraphExecDestroy(dec->graph_exec);
   if (dec->graph) (void)hipGraphDestroy(dec->graph);
   if (dec->cap_stream) (void)hipStreamDestroy(dec->cap_stream);
+  if (dec->noalloc) {
+    // Static storage: end the object's lifetime and free the GPU's slot.
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    const int dev = dec->device;
+    dec->~sb_decoder();
+    g_noalloc[dev].in_use = false;
+    return SB_OK;
+  }
   delete dec;
   return SB_OK;
 }

@@ -31,7 +31,8 @@ def _check(status: int, where: str, dec_handle=None):
         return
     detail = ""
     L = N.lib()
-    if dec_handle is not None:
+    if dec_handle is not None or where == "sb_create_noalloc":
+        # (a failed sb_create_noalloc leaves its text for a NULL decoder)
         msg = L.sb_last_error(dec_handle)
         detail = msg.decode() if msg else ""
     if not detail:
@@ -70,12 +71,15 @@ class Decoder:
 
     Weights are torch tensors on the GPU: float32, or bfloat16 for bf16
     models ([d,d], [V,d], [V,d], optional [L,2,d,d]). They must outlive the
-    decoder (the decoder keeps references)."""
+    decoder (the decoder keeps references). With noalloc=True the decoder
+    is made by sb_create_noalloc: its workspace is the library's static
+    scratch (one such decoder per GPU at a time, workspace at most
+    SB_NOALLOC_SCRATCH_BYTES) and no workspace tensor is allocated."""
 
     def __init__(self, W_h, E, W_out, *, beta: float, k: int, n: int, eps: float = 0.0,
                  delta: Optional[float] = None, M: Optional[int] = None, sched: str = "var_stream",
                  max_len_cap: int = 256, max_inputs: int = 1024, W_kv=None, stream=None,
-                 pool: Optional[int] = None, attn: bool = False):
+                 pool: Optional[int] = None, attn: bool = False, noalloc: bool = False):
         import torch
         self.torch = torch
         if not torch.cuda.is_available():
@@ -96,12 +100,18 @@ class Decoder:
                                   pool=pool)
         L = N.lib()
         _check(L.sb_validate(ctypes.byref(self.model), ctypes.byref(self.params)), "sb_validate")
-        nbytes = workspace_bytes(self.model, self.params)
-        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=W_out.device)
         h = ctypes.c_void_p()
-        _check(L.sb_create(ctypes.byref(self.model), ctypes.byref(self.params),
-                           ctypes.c_void_p(self.workspace.data_ptr()), nbytes,
-                           ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)), "sb_create")
+        if noalloc:
+            self.workspace = None
+            _check(L.sb_create_noalloc(ctypes.byref(self.model), ctypes.byref(self.params),
+                                       ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)),
+                   "sb_create_noalloc")
+        else:
+            nbytes = workspace_bytes(self.model, self.params)
+            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=W_out.device)
+            _check(L.sb_create(ctypes.byref(self.model), ctypes.byref(self.params),
+                               ctypes.c_void_p(self.workspace.data_ptr()), nbytes,
+                               ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)), "sb_create")
         self.handle = h
         self.n_submitted = 0
         self._h0_keep = []
