@@ -251,12 +251,21 @@ sb_status sb_set_timing(sb_decoder *dec, int32_t enable);
  * launches since timing was enabled. Synchronizes the stream. */
 sb_status sb_timing(sb_decoder *dec, double *proj_ms, int64_t *proj_launches);
 
-/* Debug view of one candidate slot after the last step (test support):
- * status, score, its tokens so far (up to tok_cap) and, with a KV state, its
- * KV rows [layers][2][steps][d] as bf16 bits (up to kv_cap elements). */
-/* Test support: run one decoder step (recurrence, projection, row merge)
- * on R explicit rows, outside any search. Valid only on a decoder with no
- * live beams (after create/reset/run); it leaves the decoder reset.
+sb_status sb_destroy(sb_decoder *dec);
+/* Text of the decoder's last failure; with dec == NULL, of the calling
+ * thread's last failed sb_create_noalloc. */
+const char *sb_last_error(const sb_decoder *dec);
+const char *sb_status_string(sb_status s);
+
+/* ------------------------------------------------------------------------
+ * Test support. Not part of the decoding interface: these calls expose one
+ * decoder step and one candidate slot so that tests can compare them with
+ * the oracle. They synchronize the stream and may reset the decoder.
+ * ------------------------------------------------------------------------ */
+
+/* Run one decoder step (recurrence, projection, row merge) on R explicit
+ * rows, outside any search. Valid only on a decoder with no live beams
+ * (after create/reset/run); it leaves the decoder reset.
  * h_prev: device [R][d] (model dtype); y, t, L_x: host [R] (last token,
  * 1-based emitted position, input length); R <= n*k. Outputs: h_out device
  * [R][d] (model dtype), lse host [R], top_lp host [R][k] (log-probabilities
@@ -266,15 +275,13 @@ sb_status sb_debug_expand(sb_decoder *dec, int32_t R, const void *h_prev, const 
                           const int32_t *t, const int32_t *L_x, void *h_out, double *lse,
                           double *top_lp, int32_t *top_tok);
 
+/* View of the candidate slot (beam, rank) after the last step: status,
+ * score, input id, steps taken, its tokens so far (up to tok_cap; n_tokens
+ * gets the count) and, with a KV state, its KV rows [layers][2][steps][d] as
+ * bf16 bits (up to kv_cap elements; kv may be NULL). */
 sb_status sb_debug_slot(sb_decoder *dec, int32_t beam, int32_t rank, int32_t *status,
                         double *score, int64_t *input, int32_t *steps, int32_t *tokens,
                         int32_t tok_cap, int32_t *n_tokens, uint16_t *kv, int64_t kv_cap);
-
-sb_status sb_destroy(sb_decoder *dec);
-/* Text of the decoder's last failure; with dec == NULL, of the calling
- * thread's last failed sb_create_noalloc. */
-const char *sb_last_error(const sb_decoder *dec);
-const char *sb_status_string(sb_status s);
 
 #ifdef __cplusplus
 }

@@ -14,9 +14,10 @@ namespace {
 // ---------------------------------------------------------------- K_rec
 // The recurrence GEMM is small ([R,d] x [d,d]) next to the projection, so it
 // is cut into 32 (out features) x 32 (rows) tiles to reach hundreds of
-// workgroups, and the K loop of each tile is split over the 4 waves of the
-// workgroup; the 4 partial sums are added in a fixed order (wave 0 + 1 + 2
-// + 3), so the result does not depend on which rows share the step. Operands
+// workgroups, and the K loop of each tile is split over the RSPLIT = 8 waves
+// of the workgroup (a 128-wide K slice each at d = 1024); the 8 partial sums
+// are added in a fixed order (wave 0 + 1 + ... + 7), so the result does not
+// depend on which rows share the step. Operands
 // are read straight from global memory (W_h and the states are L2/MALL
 // resident); each lane loads the 16 bytes it feeds to the MFMA.
 constexpr int RT = 32;          // tile edge

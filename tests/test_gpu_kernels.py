@@ -40,8 +40,9 @@ def _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse):
     if wl.is_bf16:
         assert np.array_equal(h_gpu, h_ref.astype(np.float32)), "bf16 states must be bit-identical"
     else:
-        # fp32 accumulation over d products: rounding error grows like
-        # sqrt(d) * 2^-24 * |pre-activation| (|pre| <~ 4): ~1e-6 at d = 1024.
+        # fp32 accumulation over d products: the rounding error grows like
+        # sqrt(d) * 2^-24 * |pre-activation| (|pre| <~ 4), ~8e-6 at d = 1024;
+        # the bound allows 8 times that (6.1e-5 at d = 1024).
         tol = 8 * np.sqrt(wl.cfg.d) * 2.0**-24 * 4
         assert np.max(np.abs(h_gpu - h_ref)) < tol
     R = lp.shape[0]
