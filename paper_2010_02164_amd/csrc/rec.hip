@@ -23,12 +23,16 @@ namespace {
 constexpr int RT = 32;          // tile edge
 constexpr int RSPLIT = 8;       // K split over the waves of a workgroup
 constexpr int RTHREADS = 64 * RSPLIT;
+// Row stride of the reduction buffer: one value more than a tile row, so
+// that the lanes of a store (consecutive rows, same feature) fall in
+// different LDS banks (a 32-value stride puts them all in one).
+constexpr int RS = RT + 1;
 
 __device__ __forceinline__ const unsigned char *rec_state_row(const DevState &st, int r, int R, int rowbytes) {
   return state_row(st, min(r, R - 1), rowbytes);
 }
 
-__device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT * RT], int vt, int rt, int R) {
+__device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT * RS], int vt, int rt, int R) {
   const int d = st.d;
   const int v0 = vt * RT, r0 = rt * RT;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -76,14 +80,14 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
 #pragma unroll
   for (int reg = 0; reg < 16; ++reg) {
     const int i = 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
-    red[w][(lane & 31) * RT + i] = acc[reg];
+    red[w][(lane & 31) * RS + i] = acc[reg];
   }
   __syncthreads();
   if (row < R) {
     float hv[2];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int o = j * RT + i0 + q;
+      const int o = j * RS + i0 + q;
       float pre = red[0][o];
 #pragma unroll
       for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
@@ -100,7 +104,7 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
 // Products of two bf16 values are exact in fp64 and so is their sum over
 // the state size in practice, so the pre-activation is accumulated with the
 // fp64 MFMA (16x16x4), tanh taken in fp64 and the result rounded once.
-__device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[RT * RT], int vt, int rt, int R) {
+__device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[RT * RS], int vt, int rt, int R) {
   const int d = st.d;
   const int v0 = vt * RT, r0 = rt * RT;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -153,14 +157,14 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int i = x * 16 + g + 4 * q, j = y * 16 + r16;
-        red[w][j * RT + i] = acc[x][y][q];
+        red[w][j * RS + i] = acc[x][y][q];
       }
   __syncthreads();
   if (row < R) {
     uint16_t hb[2];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int o = j * RT + i0 + q;
+      const int o = j * RS + i0 + q;
       double pre = red[0][o];
 #pragma unroll
       for (int x = 1; x < RSPLIT; ++x) pre += red[x][o];   // fixed order
@@ -182,7 +186,7 @@ __global__ __launch_bounds__(RTHREADS) void k_rec(DevState st) {
   const int T = (st.d / RT) * nra;
   const int x = blockIdx.x & 7, gx = gridDim.x >> 3;
   const int lo = (int)((long long)T * x / 8), hi = (int)((long long)T * (x + 1) / 8);
-  __shared__ typename std::conditional<BF16, double, float>::type red[RSPLIT][RT * RT];
+  __shared__ typename std::conditional<BF16, double, float>::type red[RSPLIT][RT * RS];
   for (int tile = lo + (int)(blockIdx.x >> 3); tile < hi; tile += gx) {
     const int vt = tile / nra, rt = tile - vt * nra;
     if constexpr (BF16)
@@ -198,7 +202,7 @@ __global__ __launch_bounds__(RTHREADS) void k_rec(DevState st) {
 hipError_t launch_rec(const DevState &st, hipStream_t s) {
   // Multiple of 8, no more than the tiles of a full step, and at most the
   // workgroups that fit on the device at once: two per compute unit for
-  // bf16 (64 KB of LDS each), four for fp32 (32 KB).
+  // bf16 (66 KB of LDS each), four for fp32 (33 KB).
   const int tiles = xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT));
   const int G = std::max(8, std::min(st.n_cu / (st.dtype == 1 ? 4 : 2) * 8, tiles));
   if (st.dtype == 1)
