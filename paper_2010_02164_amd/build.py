@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUTDIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUTDIR, "libstreambeam.so")
-SOURCES = ["api.hip", "sched.hip", "rec.hip", "proj.hip", "beam.hip", "kv.hip", "attn.hip"]
+SOURCES = ["api.hip", "sched.hip", "rec.hip", "proj.hip", "beam.hip", "attn.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -53,7 +53,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, o_pack, o_off, kvs, anc, wkvT, xbuf, attn_part, wout_t, total;
+      o_count, o_hyp, o_tok, o_pack, o_off, kvs, anc, wkv_t, xbuf, attn_part, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -123,7 +123,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
     const size_t planes = (size_t)m.kv_layers * 2;
     L.kvs = take(nk * MLC * planes * d * 2);
     L.anc = take(2 * nk * ((MLC + 3) / 4 * 4));
-    L.wkvT = take(planes * d * d * 2);
+    L.wkv_t = take(planes * d * d * 2);
   }
   if (m.attn) {
     L.xbuf = take(Rm * d * 2);
@@ -382,7 +382,7 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   if (model->kv_layers > 0) {
     st.kvs = reinterpret_cast<uint16_t *>(w + L.kvs);
     st.anc = reinterpret_cast<uint8_t *>(w + L.anc);
-    st.wkvT = reinterpret_cast<uint16_t *>(w + L.wkvT);
+    st.wkv_t = w + L.wkv_t;
   }
   st.anc_stride = (dec->params.max_len_cap + 3) / 4 * 4;
   st.attn = model->attn;
@@ -443,7 +443,7 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   if (launch_init(st, dec->stream) != hipSuccess) return SB_E_HIP;
   if (launch_relayout_wout(st, dec->stream) != hipSuccess) return SB_E_HIP;
   if (model->kv_layers > 0 &&
-      launch_transpose_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
+      launch_relayout_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
     return SB_E_HIP;
   return SB_OK;
 }

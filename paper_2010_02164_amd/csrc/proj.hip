@@ -19,6 +19,10 @@
 // sequence and adds them once, so a row's result does not depend on the
 // batch or on the tiling.
 //
+// The same tile walk, with W_kv in place of W_out and a bf16 store in place
+// of the log-sum-exp / top-k epilogue, appends each expansion's KV rows
+// (k_kv_append, below).
+//
 // W_out is streamed straight into registers from a copy laid out in MFMA
 // fragment order (one coalesced 1 KB load per wave and fragment), kept D
 // chunks ahead; the states of each half pass through a double-buffered LDS
@@ -235,11 +239,42 @@ __device__ __forceinline__ void write_record(const DevState &st, int j, int vt, 
                 __float_as_uint(rec[4 * x + 3])};
 }
 
+// KV append epilogue of one 32-row block of a wave's 32 outputs (the layout
+// of block_lists): row j's bf16(sum) values go to the KV rows of the
+// expanded candidate, at (beam, level t-1, rank), outputs o0 + 8*(reg/4) +
+// 4h + reg%4.
+__device__ __forceinline__ uint16_t bf16_rne_f(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__device__ __forceinline__ void kv_store_block(const DevState &st, const f16v &z, int o0, int h, int j, int R) {
+  if (j >= R) return;
+  const int NO = st.kv_layers * 2 * st.d;
+  const int slot = st.r_slot[j], beam = slot / st.k, rank = slot - beam * st.k;
+  uint16_t *out = st.kvs + (((size_t)beam * st.max_len_cap + (st.r_t[j] - 1)) * st.k + rank) * NO + o0 + 4 * h;
+#pragma unroll
+  for (int gq = 0; gq < 4; ++gq) {
+    u2 pk;
+    pk[0] = (uint32_t)bf16_rne_f(z[4 * gq + 0]) | ((uint32_t)bf16_rne_f(z[4 * gq + 1]) << 16);
+    pk[1] = (uint32_t)bf16_rne_f(z[4 * gq + 2]) | ((uint32_t)bf16_rne_f(z[4 * gq + 3]) << 16);
+    *reinterpret_cast<u2 *>(out + 8 * gq) = pk;
+  }
+}
+
+// Weights and rows a tile walk reads: W_out and the projection input for
+// the vocabulary projection; W_kv and the new states for the KV append.
+struct GemmOperands {
+  const unsigned char *w;   // fragment-ordered weights, 128 outputs per tile
+  const void *in;           // [R][d] rows
+};
+
 // Tile of at most 4 blocks (128 rows from r0): the K range is split in two
 // fixed halves, waves 0-3 summing the first, waves 4-7 the second; the two
 // partial sums are added once.
-template <bool BF16, int KB>
-__device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB> &sm, int vt, int r0, int R, int nbv) {
+template <bool BF16, int KB, bool KV>
+__device__ __forceinline__ void proj_tile_ksplit(const DevState &st, const GemmOperands &op, ProjSmem<KB> &sm, int vt,
+                                                 int r0, int R, int nbv) {
   const int d = st.d, V = st.V;
   const int v0 = vt * TV;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -252,7 +287,7 @@ __device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB
   const int kbeg = g * nh;
 
   // W_out fragments of this wave: chunk kt at ((vt*nk + kt)*4 + wv) * 4 KB.
-  const unsigned char *abase = st.wout_t + ((size_t)(vt * nk + kbeg) * 4 + wv) * WCH;
+  const unsigned char *abase = op.w + ((size_t)(vt * nk + kbeg) * 4 + wv) * WCH;
   // State staging: thread -> rows (tg/8) + 32u of the tile (clamped to R-1),
   // 16-byte column tg%8 of the half's chunk.
   const int tg = tid & 255;
@@ -260,7 +295,7 @@ __device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB
   uint32_t boff[NB];
 #pragma unroll
   for (int u = 0; u < NB; ++u) boff[u] = (uint32_t)min(r0 + srow + 32 * u, R - 1) * (uint32_t)rowbytes + scol;
-  const unsigned char *bbase = static_cast<const unsigned char *>(st.proj_in) + (size_t)kbeg * CH;
+  const unsigned char *bbase = static_cast<const unsigned char *>(op.in) + (size_t)kbeg * CH;
   f16v acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f16v{};
@@ -299,6 +334,13 @@ __device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB
 #pragma unroll
       for (int reg = 0; reg < 16; ++reg) own[bl][reg] += sm.red[1 - g][wv][bl][reg][lane];
     }
+  }
+
+  if constexpr (KV) {
+#pragma unroll
+    for (int bl = 0; bl < 2; ++bl)
+      if (2 * g + bl < nbv) kv_store_block(st, own[bl], v0 + 32 * wv, h, r0 + 32 * (2 * g + bl) + l32, R);
+    return;
   }
 
   // Epilogue on the owned blocks 2g + bl.
@@ -341,8 +383,9 @@ __device__ __forceinline__ void proj_tile_ksplit(const DevState &st, ProjSmem<KB
 // wave sums its blocks over the first K half and then over the second, in
 // two accumulators added once at the end: the same order of additions as a
 // K-split tile, so a row's logits do not depend on how the step was tiled.
-template <bool BF16, int KB>
-__device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &sm, int vt, int r0, int R, int nbt) {
+template <bool BF16, int KB, bool KV>
+__device__ __forceinline__ void proj_tile_big(const DevState &st, const GemmOperands &op, ProjSmem<KB> &sm, int vt,
+                                              int r0, int R, int nbt) {
   const int d = st.d, V = st.V;
   const int v0 = vt * TV;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -364,7 +407,7 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
   unsigned char (*Bt)[LS] = sm.B[0][g];
   unsigned char (*Bt1)[LS] = sm.B[1][g];
   const uint32_t alane = (uint32_t)lane * 16u;
-  const unsigned char *hb = static_cast<const unsigned char *>(st.proj_in);
+  const unsigned char *hb = static_cast<const unsigned char *>(op.in);
   f16v acc0[NB], acc1[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -375,7 +418,7 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
     const int kbeg = half * nh;
-    const unsigned char *abase = st.wout_t + ((size_t)(vt * nk + kbeg) * 4 + wv) * WCH;
+    const unsigned char *abase = op.w + ((size_t)(vt * nk + kbeg) * 4 + wv) * WCH;
     const unsigned char *bbase = hb + (size_t)kbeg * CH;
     f16v *acc = half ? acc1 : acc0;
     if (half) __syncthreads();   // the staging tile of the first half is done
@@ -385,7 +428,18 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
       proj_mainloop<BF16, 4, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
   }
 
-  if constexpr (KB == 4) {
+  if constexpr (KV) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int blk = gb0 + i;
+      if (i < nbh && blk < nbt) {
+        f16v z;
+#pragma unroll
+        for (int reg = 0; reg < 16; ++reg) z[reg] = acc0[i][reg] + acc1[i][reg];
+        kv_store_block(st, z, v0 + 32 * wv, h, r0 + 32 * blk + l32, R);
+      }
+    }
+  } else if constexpr (KB == 4) {
     // Epilogue: the lane lists of every owned block, then wave i of each
     // group merges block i's four vocabulary slices, all blocks at once.
 #pragma unroll
@@ -463,8 +517,9 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, ProjSmem<KB> &
 // the sums are the same. vw: 256-row vocabulary tile; its second 128-row
 // half may lie past the vocabulary (odd tile count): those waves compute a
 // copy of the last tile and write nothing.
-template <int KB>
-__device__ __forceinline__ void proj_tile_wide(const DevState &st, ProjSmem<KB> &sm, int vw, int r0, int R) {
+template <int KB, bool KV>
+__device__ __forceinline__ void proj_tile_wide(const DevState &st, const GemmOperands &op, ProjSmem<KB> &sm, int vw,
+                                               int r0, int R, int nvt) {
   const int d = st.d, V = st.V;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -473,16 +528,16 @@ __device__ __forceinline__ void proj_tile_wide(const DevState &st, ProjSmem<KB> 
   const int rowbytes = d * 2;
   const int nk = rowbytes / CH, nh = nk >> 1, kbeg = g * nh;
   const int t2 = vq >> 1;                          // which 128-row half of the 256
-  const int vt = min(2 * vw + t2, st.S - 1);       // 128-row tile of this wave's rows
+  const int vt = min(2 * vw + t2, nvt - 1);        // 128-row tile of this wave's rows
   const int s0 = 2 * (vq & 1);                     // its first slice in that tile
   const int v0 = vt * TV;
-  const unsigned char *abase = st.wout_t + ((size_t)(vt * nk + kbeg) * 4 + s0) * WCH;
+  const unsigned char *abase = op.w + ((size_t)(vt * nk + kbeg) * 4 + s0) * WCH;
   const int tg = tid & 255;
   const int srow = tg >> 3, scol = (tg & 7) * 16;
   uint32_t boff[NB];
 #pragma unroll
   for (int u = 0; u < NB; ++u) boff[u] = (uint32_t)min(r0 + srow + 32 * u, R - 1) * (uint32_t)rowbytes + scol;
-  const unsigned char *bbase = static_cast<const unsigned char *>(st.proj_in) + (size_t)kbeg * CH;
+  const unsigned char *bbase = static_cast<const unsigned char *>(op.in) + (size_t)kbeg * CH;
   f16v acc[2 * NB];
 #pragma unroll
   for (int b = 0; b < 2 * NB; ++b) acc[b] = f16v{};
@@ -507,6 +562,17 @@ __device__ __forceinline__ void proj_tile_wide(const DevState &st, ProjSmem<KB> 
 #pragma unroll
       for (int reg = 0; reg < 16; ++reg) own[x][bl][reg] += sm.red[1 - g][vq][bl][reg][lane];
     __syncthreads();
+  }
+
+  if constexpr (KV) {
+    if (2 * vw + t2 < nvt) {
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int bl = 0; bl < 2; ++bl)
+          kv_store_block(st, own[x][bl], v0 + 32 * (s0 + x), h, r0 + 32 * (2 * g + bl) + l32, R);
+    }
+    return;
   }
 
   // Lane lists of the four owned (slice, block) tiles, then wave w merges
@@ -542,14 +608,15 @@ __device__ __forceinline__ void proj_tile_wide(const DevState &st, ProjSmem<KB> 
 
 // Row tile rt covers blocks bt*rt .. bt*rt + bt - 1 (32 rows each) of
 // vocabulary tile vt.
-template <bool BF16, int KB>
-__device__ __forceinline__ void proj_tile(const DevState &st, ProjSmem<KB> &sm, int vt, int rt, int R, int bt) {
+template <bool BF16, int KB, bool KV>
+__device__ __forceinline__ void proj_tile(const DevState &st, const GemmOperands &op, ProjSmem<KB> &sm, int vt, int rt,
+                                          int R, int bt) {
   const int r0 = rt * bt * 32;
   const int nbt = min(bt, (R - r0 + 31) >> 5);   // blocks holding valid rows
   if (nbt <= NB)
-    proj_tile_ksplit<BF16, KB>(st, sm, vt, r0, R, nbt);
+    proj_tile_ksplit<BF16, KB, KV>(st, op, sm, vt, r0, R, nbt);
   else
-    proj_tile_big<BF16, KB>(st, sm, vt, r0, R, nbt);
+    proj_tile_big<BF16, KB, KV>(st, op, sm, vt, r0, R, nbt);
 }
 
 // Blocks per row tile for a step of R rows: the count (1..8) that minimizes
@@ -583,16 +650,16 @@ __device__ __forceinline__ int row_tile_blocks(int R, int S, int G) {
 // tiles holding rows of this step are visited, and no workgroup is launched
 // just to exit (idle ones would occupy compute units that the dispatcher
 // then withholds from working ones).
-template <bool BF16, int KB>
-__global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
+template <bool BF16, int KB, bool KV>
+__device__ __forceinline__ void tile_walk(const DevState &st, const GemmOperands &op, int nvt) {
   const int R = st.ctrl->R;
   if (R <= 0) return;
   // bf16 steps whose 256-wide tiles fill at least one round use them.
-  const int S2 = (st.S + 1) >> 1, nrw = (R + TR - 1) / TR;
+  const int S2 = (nvt + 1) >> 1, nrw = (R + TR - 1) / TR;
   const bool wide = BF16 && KB == 4 && S2 * nrw >= (int)gridDim.x;
-  const int bt = wide ? NB : row_tile_blocks(R, st.S, (int)gridDim.x);
+  const int bt = wide ? NB : row_tile_blocks(R, nvt, (int)gridDim.x);
   const int nra = wide ? nrw : (R + 32 * bt - 1) / (32 * bt);
-  const int T = (wide ? S2 : st.S) * nra;
+  const int T = (wide ? S2 : nvt) * nra;
   const int x = blockIdx.x & 7, gx = gridDim.x >> 3, j = blockIdx.x >> 3;
   const int lo = (int)((long long)T * x / 8), nt = (int)((long long)T * (x + 1) / 8) - lo;
   __shared__ ProjSmem<KB> sm;
@@ -603,14 +670,28 @@ __global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
     const int vt = tile / nra, rt = tile - vt * nra;
     if constexpr (BF16 && KB == 4) {
       if (wide) {
-        proj_tile_wide<KB>(st, sm, vt, rt * TR, R);
+        proj_tile_wide<KB, KV>(st, op, sm, vt, rt * TR, R, nvt);
         __syncthreads();   // LDS is reused by the next tile
         continue;
       }
     }
-    proj_tile<BF16, KB>(st, sm, vt, rt, R, bt);
+    proj_tile<BF16, KB, KV>(st, op, sm, vt, rt, R, bt);
     __syncthreads();   // LDS is reused by the next tile
   }
+}
+
+template <bool BF16, int KB>
+__global__ __launch_bounds__(THREADS, 1) void k_proj(DevState st) {
+  tile_walk<BF16, KB, false>(st, GemmOperands{st.wout_t, st.proj_in}, st.S);
+}
+
+// KV rows of every expansion of the step: bf16(h . W_kv[l][j]) for the
+// L*2*d outputs, the [R,d] x [d, L*2*d] product on the projection's tiles
+// and K order (K halves summed apart and added once, so a row's KV values do
+// not depend on the rows sharing the step), stored at the candidate's
+// (beam, level, rank) place (App. A.2's incremental decoder state).
+__global__ __launch_bounds__(THREADS, 1) void k_kv_append(DevState st) {
+  tile_walk<true, 4, true>(st, GemmOperands{st.wkv_t, st.hbuf}, st.kv_layers * 2 * st.d / TV);
 }
 
 // W_out [V][d] -> MFMA fragment order [S][nk][4 slices][4 pieces][64 lanes][16 B]:
@@ -631,6 +712,33 @@ __global__ void k_relayout_wout(const unsigned char *__restrict__ src, unsigned 
     u4 val = {0u, 0u, 0u, 0u};
     if (v < V)
       val = *reinterpret_cast<const u4 *>(src + (size_t)v * rowbytes + (size_t)kt * CH + 64 * (ln >> 5) + 16 * q);
+    *reinterpret_cast<u4 *>(dst + p * 16) = val;
+  }
+}
+
+// W_kv [L][2][d_in][d_out] -> the same fragment order, output feature
+// v = plane * d + o (plane = 2l + j) in place of the vocabulary row: lane
+// (h, l) of slice s at piece q holds the 8 bf16 values W_kv[plane][k0 + e][o],
+// k0 = kt*64 + 32h + 8q, e < 8, of output v = 128*vt + 32s + l.
+__global__ void k_relayout_wkv(const uint16_t *__restrict__ W, unsigned char *__restrict__ dst, int d, int NO) {
+  const int nk = d * 2 / CH;
+  const size_t pieces = (size_t)(NO / TV) * nk * 4 * 4 * 64;
+  for (size_t p = (size_t)blockIdx.x * blockDim.x + threadIdx.x; p < pieces; p += (size_t)gridDim.x * blockDim.x) {
+    const int ln = (int)(p & 63);
+    const int q = (int)((p >> 6) & 3);
+    const int s = (int)((p >> 8) & 3);
+    const size_t vk = p >> 10;
+    const int kt = (int)(vk % nk);
+    const int vt = (int)(vk / nk);
+    const int v = vt * TV + 32 * s + (ln & 31);
+    const int plane = v / d, o = v - plane * d;
+    const int k0 = kt * (CH / 2) + 32 * (ln >> 5) + 8 * q;
+    const uint16_t *src = W + ((size_t)plane * d + k0) * d + o;
+    uint16_t e[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) e[i] = src[(size_t)i * d];
+    u4 val = {(uint32_t)e[0] | ((uint32_t)e[1] << 16), (uint32_t)e[2] | ((uint32_t)e[3] << 16),
+              (uint32_t)e[4] | ((uint32_t)e[5] << 16), (uint32_t)e[6] | ((uint32_t)e[7] << 16)};
     *reinterpret_cast<u4 *>(dst + p * 16) = val;
   }
 }
@@ -660,6 +768,19 @@ hipError_t launch_relayout_wout(const DevState &st, hipStream_t s) {
 
 hipError_t launch_proj(const DevState &st, hipStream_t s) {
   return st.dtype == 1 ? launch_proj_t<true>(st, s) : launch_proj_t<false>(st, s);
+}
+
+hipError_t launch_kv_append(const DevState &st, hipStream_t s) {
+  // Sized like the projection's grid, over the L*2*d/128 output tiles.
+  const int nvt = st.kv_layers * 2 * st.d / TV;
+  const int G = std::max(8, std::min(st.n_cu / 8 * 8, xcd_grid(nvt * ((st.R_max + 31) / 32))));
+  hipLaunchKernelGGL(k_kv_append, dim3(G), dim3(THREADS), 0, s, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_relayout_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s) {
+  hipLaunchKernelGGL(k_relayout_wkv, dim3(2048), dim3(256), 0, s, W_kv, st.wkv_t, st.d, st.kv_layers * 2 * st.d);
+  return hipGetLastError();
 }
 
 }  // namespace sb

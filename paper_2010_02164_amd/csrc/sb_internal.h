@@ -84,7 +84,7 @@ struct DevState {
   // keeps in anc (two buffers, the beam's parity picks the current one).
   uint16_t *kvs;       // [n][max_len_cap][k][L*2][d]
   uint8_t *anc;        // [2][n*k][anc_stride]: rank of the ancestor at each level
-  uint16_t *wkvT;      // [L*2*d][d]  (transposed W_kv: out-feature major)
+  unsigned char *wkv_t; // W_kv in the fragment order of wout_t: output v = plane*d + o as vocabulary row
   // attention read-out (attn models): projection input x [R_max][d] bf16
   void *xbuf;
   double *attn_part;   // [R_max][L][d] per-layer read-outs a_l
@@ -130,6 +130,6 @@ hipError_t launch_backtrack(const DevState &st, int q0, int q1, hipStream_t s);
 hipError_t launch_pack(const DevState &st, int q0, int q1, hipStream_t s);
 hipError_t launch_init(const DevState &st, hipStream_t s);
 hipError_t launch_relayout_wout(const DevState &st, hipStream_t s);
-hipError_t launch_transpose_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s);
+hipError_t launch_relayout_wkv(const DevState &st, const uint16_t *W_kv, hipStream_t s);
 
 }  // namespace sb
