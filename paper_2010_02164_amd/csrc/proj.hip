@@ -379,10 +379,13 @@ __device__ __forceinline__ void proj_tile_ksplit(const DevState &st, const GemmO
 }
 
 // Tile of 5 to 8 blocks (rows r0 .. r0+255): the blocks are split between
-// the two wave groups (nbh each, the last block possibly padding), and every
-// wave sums its blocks over the first K half and then over the second, in
-// two accumulators added once at the end: the same order of additions as a
-// K-split tile, so a row's logits do not depend on how the step was tiled.
+// the two wave groups (group 0 takes nbh = ceil(nbt/2), group 1 the other
+// nbt - nbh, so an odd count leaves group 1 one block short rather than
+// computing a padding block: the two waves that share a SIMD then issue
+// nbt blocks' MFMAs, not 2 nbh), and every wave sums its blocks over the
+// first K half and then over the second, in two accumulators added once at
+// the end: the same order of additions as a K-split tile, so a row's
+// logits do not depend on how the step was tiled.
 template <bool BF16, int KB, bool KV>
 __device__ __forceinline__ void proj_tile_big(const DevState &st, const GemmOperands &op, ProjSmem<KB> &sm, int vt,
                                               int r0, int R, int nbt) {
@@ -395,7 +398,8 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, const GemmOper
   const int rowbytes = d * (BF16 ? 2 : 4);
   const int nk = rowbytes / CH;
   const int nh = nk >> 1;
-  const int nbh = (nbt + 1) >> 1;                 // blocks per group (3 or 4)
+  const int nbh = (nbt + 1) >> 1;                 // blocks of group 0 (3 or 4)
+  const int nbg = g ? nbt - nbh : nbh;            // blocks of this group (2 to 4)
   const int gb0 = g * nbh;                        // first block of this group
 
   const int tg = tid & 255;
@@ -422,7 +426,10 @@ __device__ __forceinline__ void proj_tile_big(const DevState &st, const GemmOper
     const unsigned char *bbase = hb + (size_t)kbeg * CH;
     f16v *acc = half ? acc1 : acc0;
     if (half) __syncthreads();   // the staging tile of the first half is done
-    if (nbh == 3)
+    // Both instantiations pass the same barriers (one per chunk).
+    if (nbg == 2)
+      proj_mainloop<BF16, 2, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
+    else if (nbg == 3)
       proj_mainloop<BF16, 3, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
     else
       proj_mainloop<BF16, 4, 2>(Bt, Bt1, abase, alane, bbase, boff, srow, scol, nh, l32, h, acc);
@@ -621,8 +628,8 @@ __device__ __forceinline__ void proj_tile(const DevState &st, const GemmOperands
 
 // Blocks per row tile for a step of R rows: the count (1..8) that minimizes
 // rounds x tile cost, where a round is one tile per workgroup and a tile
-// costs its MFMA blocks (a big tile computes an even count) plus a fixed
-// part worth 0.7 block (prologue, epilogue). Ties go to the larger tile.
+// costs its MFMA blocks plus a fixed part worth 0.7 block (prologue,
+// epilogue). Ties go to the larger tile.
 __device__ __forceinline__ int row_tile_blocks(int R, int S, int G) {
   const int B = (R + 31) >> 5;
   int best_bt = NB;
@@ -631,7 +638,7 @@ __device__ __forceinline__ int row_tile_blocks(int R, int S, int G) {
     const int nra = (B + bt - 1) / bt;
     const int be = min(bt, B);
     const int rounds = (S * nra + G - 1) / G;
-    const float cost = (float)rounds * ((float)(be <= NB ? be : 2 * ((be + 1) >> 1)) + 0.7f);
+    const float cost = (float)rounds * ((float)be + 0.7f);
     if (cost <= best) {
       best = cost;
       best_bt = bt;
