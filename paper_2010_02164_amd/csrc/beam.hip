@@ -16,6 +16,7 @@
 //                Continuing beams get their new candidates' states.
 //   K_backtrack: rebuild each finished hypothesis's tokens from the
 //                backpointer history, one thread per hypothesis.
+#include "mfma_common.h"
 #include "sb_internal.h"
 #include "topk.h"
 #include "wave.h"
@@ -74,48 +75,79 @@ __device__ __forceinline__ void wave_lse(float &m, float &s) {
   lse_stage<5>(m, s);
 }
 
-// Logit z[v] of one row recomputed from W_out and the row's projection
-// input (fp32 accumulation), with the EOS bias of token 0. fp32 follows the
+// Logit z[v] of one fp32 row recomputed from W_out and the row's
+// projection input, with the EOS bias of token 0. It follows the
 // projection's arithmetic exactly: each K half in chunks of 32 values, and
 // per chunk, piece q and element e the two fused products of k and k + 16
 // (an fp32 32x32x2 MFMA adds its two products to the sum one after the
 // other, lane half 0's first), then the halves added once, so a recomputed
-// logit equals the projection's bit for bit. bf16 sums the same products
-// in plain order (the bf16 MFMA's internal rounding is not reproduced).
-__device__ __forceinline__ float recompute_logit(const DevState &st, int row, int v) {
+// logit equals the projection's bit for bit.
+__device__ __forceinline__ float recompute_logit_f32(const DevState &st, int row, int v) {
   const int d = st.d;
-  float z = 0.0f;
-  if (st.dtype == 1) {
-    const uint4 *w = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(st.W_out) + (size_t)v * d);
-    const uint4 *x = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(st.proj_in) + (size_t)row * d);
-    for (int c = 0; c < d / 8; ++c) {
-      const uint4 a = w[c], b = x[c];
-      const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        z = fmaf(__uint_as_float(aw[e] << 16), __uint_as_float(bw[e] << 16), z);
-        z = fmaf(__uint_as_float(aw[e] & 0xFFFF0000u), __uint_as_float(bw[e] & 0xFFFF0000u), z);
-      }
-    }
-  } else {
-    const float *w = static_cast<const float *>(st.W_out) + (size_t)v * d;
-    const float *x = static_cast<const float *>(st.proj_in) + (size_t)row * d;
-    float half[2];
-    for (int g = 0; g < 2; ++g) {
-      float acc = 0.0f;
-      for (int c = g * (d / 2); c < (g + 1) * (d / 2); c += 32)
-        for (int q = 0; q < 4; ++q)
-          for (int e = 0; e < 4; ++e) {
-            const int k0 = c + 4 * q + e;
-            acc = fmaf(w[k0], x[k0], acc);
-            acc = fmaf(w[k0 + 16], x[k0 + 16], acc);
-          }
-      half[g] = acc;
-    }
-    z = half[0] + half[1];
+  const float *w = static_cast<const float *>(st.W_out) + (size_t)v * d;
+  const float *x = static_cast<const float *>(st.proj_in) + (size_t)row * d;
+  float half[2];
+  for (int g = 0; g < 2; ++g) {
+    float acc = 0.0f;
+    for (int c = g * (d / 2); c < (g + 1) * (d / 2); c += 32)
+      for (int q = 0; q < 4; ++q)
+        for (int e = 0; e < 4; ++e) {
+          const int k0 = c + 4 * q + e;
+          acc = fmaf(w[k0], x[k0], acc);
+          acc = fmaf(w[k0 + 16], x[k0 + 16], acc);
+        }
+    half[g] = acc;
   }
+  float z = half[0] + half[1];
   if (v == 0) z += st.beta * (float)(st.r_t[row] - st.r_Lx[row]);
   return z;
+}
+
+// bf16: the 128 logits of vocabulary tile vt for one row, recomputed by the
+// projection's own MFMA sequence so that they equal its logits bit for bit
+// (the bf16 MFMA's internal rounding is not modelled, it is replayed): per
+// 32-row slice, each K half accumulated chunk by chunk and piece by piece
+// from the same W_out fragments and state bytes, then the halves added
+// once. Every column of the MFMA gets the row's state, so all 32 columns
+// hold the same logits; lane (h, l) with l < 16 inserts the logit of
+// register l, vocabulary row 32s + 8(l/4) + 4h + l%4 of the tile, into its
+// list (each of the 128 logits once).
+template <int KB>
+__device__ __forceinline__ void recompute_tile_bf16(const DevState &st, int row, int vt, int lane, TopK<KB> &tk) {
+  constexpr int CH = 128, FRAG = 1024;
+  const int nk = st.d * 2 / CH, nh = nk >> 1;
+  const int h = lane >> 5, l32 = lane & 31;
+  const unsigned char *x = static_cast<const unsigned char *>(st.proj_in) + (size_t)row * st.d * 2 + 64 * h;
+  const float bias = st.beta * (float)(st.r_t[row] - st.r_Lx[row]);
+#pragma unroll 1
+  for (int s = 0; s < 4; ++s) {
+    f16v half[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      f16v acc = {};
+#pragma unroll 1
+      for (int c = g * nh; c < (g + 1) * nh; ++c) {
+        const unsigned char *a = st.wout_t + ((size_t)(vt * nk + c) * 4 + s) * 4 * FRAG + lane * 16;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const u4 av = *reinterpret_cast<const u4 *>(a + q * FRAG);
+          const u4 bv = *reinterpret_cast<const u4 *>(x + c * CH + 16 * q);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, av), __builtin_bit_cast(bf8, bv), acc,
+                                                        0, 0, 0);
+        }
+      }
+      half[g] = acc;
+    }
+    if (l32 < 16) {
+      float z = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (r == l32) z = half[0][r] + half[1][r];
+      const int v = vt * 128 + 32 * s + 8 * (l32 >> 2) + 4 * h + (l32 & 3);
+      if (v == 0) z += bias;
+      if (v < st.V) topk_insert(tk, make_key(z, v));
+    }
+  }
 }
 
 // Merge the per-tile partials of one row (one wave). Each lane folds the
@@ -259,10 +291,14 @@ __device__ __forceinline__ double merge_row(const DevState &st, int row, int lan
       const int src = __ffsll((long long)mask) - 1;
       mask &= mask - 1;
       const int vt = t0 + src;
+      if (st.dtype == 1) {
+        recompute_tile_bf16<KB>(st, row, vt, lane, tk);
+      } else {
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int v = vt * 128 + 64 * half + lane;
-        if (v < st.V) topk_insert(tk, make_key(recompute_logit(st, row, v), v));
+        for (int half = 0; half < 2; ++half) {
+          const int v = vt * 128 + 64 * half + lane;
+          if (v < st.V) topk_insert(tk, make_key(recompute_logit_f32(st, row, v), v));
+        }
       }
     }
   }
