@@ -53,7 +53,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, o_pack, o_off, kvs, anc, wkv_t, xbuf, attn_part, wout_t, total;
+      o_count, o_hyp, o_tok, o_pack, o_off, wh_t, kvs, anc, wkv_t, xbuf, attn_part, wout_t, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -119,6 +119,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.o_pack = take(Q * k * MLC * 4);
   L.o_off = take(Q * k * 8);
   L.wout_t = take(S * 128 * d * es);
+  if (m.dtype == SB_F32) L.wh_t = take(d * d * 4);
   if (m.kv_layers > 0) {
     const size_t planes = (size_t)m.kv_layers * 2;
     L.kvs = take(nk * MLC * planes * d * 2);
@@ -393,6 +394,7 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   st.E = model->E;
   st.W_out = model->W_out;
   st.wout_t = w + L.wout_t;
+  st.wh_t = model->dtype == SB_F32 ? reinterpret_cast<const float4 *>(w + L.wh_t) : nullptr;
   const sb_params &p = dec->params;
   st.n = pool_of(p);
   st.k = p.k;
@@ -442,6 +444,7 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   }
   if (launch_init(st, dec->stream) != hipSuccess) return SB_E_HIP;
   if (launch_relayout_wout(st, dec->stream) != hipSuccess) return SB_E_HIP;
+  if (launch_relayout_wh(st, dec->stream) != hipSuccess) return SB_E_HIP;
   if (model->kv_layers > 0 &&
       launch_relayout_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
     return SB_E_HIP;

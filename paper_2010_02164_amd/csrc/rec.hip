@@ -49,7 +49,9 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
     ev[0] = E[0];
     ev[1] = E[1];
   }
-  const float *arow = static_cast<const float *>(st.W_h) + (size_t)(v0 + (lane & 31)) * d + w * kq;
+  // A: this wave's K slice of the fragment-ordered W_h copy, one coalesced
+  // 1 KB block per 8 K values (lane (h, l): row v0 + l, K + 4h .. +3).
+  const f4 *afr = reinterpret_cast<const f4 *>(st.wh_t) + ((size_t)vt * (d / 8) + (w * kq) / 8) * 64 + lane;
   const float *brow = reinterpret_cast<const float *>(rec_state_row(st, r0 + (lane & 31), R, rowbytes)) + w * kq;
   const int h = (lane >> 5) * 4;
   f16v acc = {};
@@ -61,7 +63,7 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
     f4 a[16], b[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      a[i] = *reinterpret_cast<const f4 *>(arow + kk + 8 * i + h);
+      a[i] = afr[(size_t)(kk / 8 + i) * 64];
       b[i] = *reinterpret_cast<const f4 *>(brow + kk + 8 * i + h);
     }
 #pragma unroll
@@ -71,7 +73,7 @@ __device__ __forceinline__ void rec_tile_f32(const DevState &st, float (*red)[RT
   }
 #pragma unroll 8
   for (; kk < kq; kk += 8) {
-    const f4 a = *reinterpret_cast<const f4 *>(arow + kk + h);
+    const f4 a = afr[(size_t)(kk / 8) * 64];
     const f4 b = *reinterpret_cast<const f4 *>(brow + kk + h);
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc, 0, 0, 0);
@@ -197,7 +199,25 @@ __global__ __launch_bounds__(RTHREADS) void k_rec(DevState st) {
   }
 }
 
+// fp32 W_h [d][d] -> the A-fragment order of rec_tile_f32 (above).
+__global__ void k_relayout_wh(const float *__restrict__ W, f4 *__restrict__ dst, int d) {
+  const size_t n = (size_t)(d / 32) * (d / 8) * 64;
+  for (size_t p = (size_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += (size_t)gridDim.x * blockDim.x) {
+    const int ln = (int)(p & 63);
+    const size_t vs = p >> 6;
+    const int s = (int)(vs % (d / 8)), vt = (int)(vs / (d / 8));
+    dst[p] = *reinterpret_cast<const f4 *>(W + (size_t)(vt * 32 + (ln & 31)) * d + 8 * s + 4 * (ln >> 5));
+  }
+}
+
 }  // namespace
+
+hipError_t launch_relayout_wh(const DevState &st, hipStream_t s) {
+  if (st.dtype == 1) return hipSuccess;
+  hipLaunchKernelGGL(k_relayout_wh, dim3(1024), dim3(256), 0, s, static_cast<const float *>(st.W_h),
+                     reinterpret_cast<f4 *>(const_cast<float4 *>(st.wh_t)), st.d);
+  return hipGetLastError();
+}
 
 hipError_t launch_rec(const DevState &st, hipStream_t s) {
   // Multiple of 8, no more than the tiles of a full step, and at most the

@@ -89,6 +89,9 @@ struct DevState {
   void *xbuf;
   double *attn_part;   // [R_max][L][d] per-layer read-outs a_l
   const void *proj_in; // rows the projection reads: xbuf (attn) or hbuf
+  // fp32 W_h in the recurrence's A-fragment order: [d/32][d/8][64 lanes][16 B],
+  // lane (h, l) of output tile vt at K step s holding W_h[32 vt + l][8 s + 4h .. +3]
+  const float4 *wh_t;
   // model
   const void *W_h, *E, *W_out;
   // W_out re-laid out tile-contiguous: [S][nk][128 rows][128 bytes], one
@@ -121,6 +124,7 @@ inline int proj_tiles(int V) { return (V + GEMM_BV - 1) / GEMM_BV; }
 // Launchers (each returns the launch status).
 hipError_t launch_sched(const DevState &st, hipStream_t s);
 hipError_t launch_rec(const DevState &st, hipStream_t s);
+hipError_t launch_relayout_wh(const DevState &st, hipStream_t s);
 hipError_t launch_proj(const DevState &st, hipStream_t s);
 hipError_t launch_rowmerge(const DevState &st, hipStream_t s);
 hipError_t launch_beam(const DevState &st, hipStream_t s);
