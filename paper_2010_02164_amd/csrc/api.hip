@@ -119,7 +119,7 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   L.o_pack = take(Q * k * MLC * 4);
   L.o_off = take(Q * k * 8);
   L.wout_t = take(S * 128 * d * es);
-  if (m.dtype == SB_F32) L.wh_t = take(d * d * 4);
+  L.wh_t = take(d * d * es);   // W_h in the recurrence's fragment order
   if (m.kv_layers > 0) {
     const size_t planes = (size_t)m.kv_layers * 2;
     L.kvs = take(nk * MLC * planes * d * 2);
@@ -395,6 +395,7 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   st.W_out = model->W_out;
   st.wout_t = w + L.wout_t;
   st.wh_t = model->dtype == SB_F32 ? reinterpret_cast<const float4 *>(w + L.wh_t) : nullptr;
+  st.wh16_t = model->dtype == SB_BF16 ? reinterpret_cast<const uint2 *>(w + L.wh_t) : nullptr;
   const sb_params &p = dec->params;
   st.n = pool_of(p);
   st.k = p.k;

@@ -120,8 +120,9 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
     ev = *reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(st.E) + (size_t)st.r_y[row] * d + v0 + i0);
   // A: 2 blocks of 16 out features, B: 2 blocks of 16 rows; the lane feeds
   // 4 consecutive bf16 at k = kk + 4g to 4 MFMAs (same permutation for A, B).
-  const uint16_t *a0 = static_cast<const uint16_t *>(st.W_h) + (size_t)(v0 + r16) * d + w * kq + 4 * g;
-  const uint16_t *a1 = a0 + (size_t)16 * d;
+  // A from the fragment-ordered bf16 W_h copy: one coalesced 512-byte block
+  // per row half and 16 K values.
+  const u2 *afr = reinterpret_cast<const u2 *>(st.wh16_t) + ((size_t)vt * (d / 16) + (w * kq) / 16) * 128 + lane;
   const uint16_t *b0 = reinterpret_cast<const uint16_t *>(rec_state_row(st, r0 + r16, R, rowbytes)) + w * kq + 4 * g;
   const uint16_t *b1 = reinterpret_cast<const uint16_t *>(rec_state_row(st, r0 + 16 + r16, R, rowbytes)) + w * kq + 4 * g;
   d4 acc[2][2];
@@ -138,8 +139,8 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
 #pragma unroll 4
   for (int kk = 0; kk < kq; kk += 16) {
     double a[2][4], b[2][4];
-    cvt(*reinterpret_cast<const u2 *>(a0 + kk), a[0]);
-    cvt(*reinterpret_cast<const u2 *>(a1 + kk), a[1]);
+    cvt(afr[(size_t)(kk / 16) * 128], a[0]);
+    cvt(afr[(size_t)(kk / 16) * 128 + 64], a[1]);
     cvt(*reinterpret_cast<const u2 *>(b0 + kk), b[0]);
     cvt(*reinterpret_cast<const u2 *>(b1 + kk), b[1]);
 #pragma unroll
@@ -210,12 +211,26 @@ __global__ void k_relayout_wh(const float *__restrict__ W, f4 *__restrict__ dst,
   }
 }
 
+// bf16 W_h [d][d] -> the A-fragment order of rec_tile_bf16 (above).
+__global__ void k_relayout_wh16(const uint16_t *__restrict__ W, u2 *__restrict__ dst, int d) {
+  const size_t n = (size_t)(d / 32) * (d / 16) * 128;
+  for (size_t p = (size_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += (size_t)gridDim.x * blockDim.x) {
+    const int ln = (int)(p & 63), x = (int)((p >> 6) & 1);
+    const size_t vs = p >> 7;
+    const int s = (int)(vs % (d / 16)), vt = (int)(vs / (d / 16));
+    dst[p] = *reinterpret_cast<const u2 *>(W + (size_t)(vt * 32 + 16 * x + (ln & 15)) * d + 16 * s + 4 * (ln >> 4));
+  }
+}
+
 }  // namespace
 
 hipError_t launch_relayout_wh(const DevState &st, hipStream_t s) {
-  if (st.dtype == 1) return hipSuccess;
-  hipLaunchKernelGGL(k_relayout_wh, dim3(1024), dim3(256), 0, s, static_cast<const float *>(st.W_h),
-                     reinterpret_cast<f4 *>(const_cast<float4 *>(st.wh_t)), st.d);
+  if (st.dtype == 1)
+    hipLaunchKernelGGL(k_relayout_wh16, dim3(1024), dim3(256), 0, s, static_cast<const uint16_t *>(st.W_h),
+                       reinterpret_cast<u2 *>(const_cast<uint2 *>(st.wh16_t)), st.d);
+  else
+    hipLaunchKernelGGL(k_relayout_wh, dim3(1024), dim3(256), 0, s, static_cast<const float *>(st.W_h),
+                       reinterpret_cast<f4 *>(const_cast<float4 *>(st.wh_t)), st.d);
   return hipGetLastError();
 }
 

@@ -91,7 +91,10 @@ struct DevState {
   const void *proj_in; // rows the projection reads: xbuf (attn) or hbuf
   // fp32 W_h in the recurrence's A-fragment order: [d/32][d/8][64 lanes][16 B],
   // lane (h, l) of output tile vt at K step s holding W_h[32 vt + l][8 s + 4h .. +3]
+  // bf16 W_h likewise for the fp64 recurrence: [d/32][d/16][2 row halves][64 lanes][8 B],
+  // lane (g, l) of half x at K step s holding W_h[32 vt + 16 x + l][16 s + 4g .. +3]
   const float4 *wh_t;
+  const uint2 *wh16_t;
   // model
   const void *W_h, *E, *W_out;
   // W_out re-laid out tile-contiguous: [S][nk][128 rows][128 bytes], one
