@@ -152,3 +152,48 @@ def test_exact_ties_follow_rank_key(gpu, cfg_i, over, pairs, sched, kw):
     rep, g, st, o = check_parity(wl, sched, max_excused=len(wl.Lx) // 3, **kw)
     tied = sum(1 for y in o.hyps for i in range(len(y)) for j in range(i + 1, len(y)) if y[i].score == y[j].score)
     assert tied > 0                                  # the ties reach the outputs
+
+
+def test_collect_in_pieces_through_the_c_abi(gpu):
+    # sb_collect with buffers too small for everything: each call returns
+    # whole inputs (SB_E_TRUNCATED while some remain), the tokens of its
+    # hypotheses packed from offset 0 of the caller's buffer; the pieces
+    # together equal a single collect of the same decode.
+    import ctypes
+
+    import numpy as np
+    import torch
+    from paper_2010_02164_amd import _native as N
+    from paper_2010_02164_amd import decoder_for_workload, inputs_to_device
+    wl = make_workload(scaled(1, N=24))
+    ref_dec = decoder_for_workload(wl, sched="var_stream")
+    ref_dec.submit(inputs_to_device(wl), wl.Lx, wl.max_len)
+    ref_dec.run()
+    ref = ref_dec.collect()
+    ref_dec.close()
+    dec = decoder_for_workload(wl, sched="var_stream")
+    dec.submit(inputs_to_device(wl), wl.Lx, wl.max_len)
+    dec.run()
+    L = N.lib()
+    got, calls, truncated = [], 0, 0
+    while True:
+        hyps = (N.SbHyp * 7)()
+        toks = np.full(400, -7, np.int32)
+        nh, nt = ctypes.c_int64(0), ctypes.c_int64(0)
+        st = L.sb_collect(dec.handle, hyps, 7, toks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 400,
+                          ctypes.byref(nh), ctypes.byref(nt))
+        calls += 1
+        assert st in (N.SB_OK, N.SB_E_TRUNCATED)
+        truncated += st == N.SB_E_TRUNCATED
+        assert nt.value == sum(hyps[i].length for i in range(nh.value))
+        assert (toks[nt.value:] == -7).all()          # nothing written past the returned tokens
+        for i in range(nh.value):
+            h = hyps[i]
+            got.append((int(h.input), int(h.rank), tuple(toks[h.tok_offset:h.tok_offset + h.length].tolist()),
+                        float(h.score), int(h.status)))
+        if st == N.SB_OK or nh.value == 0:
+            break
+    torch.cuda.synchronize()
+    dec.close()
+    assert truncated > 0 and calls > 2
+    assert got == [(h.input, h.rank, h.tokens, h.score, h.status) for h in ref]
