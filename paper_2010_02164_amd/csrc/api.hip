@@ -53,10 +53,15 @@ constexpr size_t ALIGN = 256;
 struct Layout {
   size_t ctrl, q_h0, q_Lx, q_ml, b_input, b_steps, b_sel, b_par, b_ml, b_nout, b_order, s_status, s_score, s_tok, s_h,
       s_row, bp, r_slot, r_hsrc, r_y, r_t, r_Lx, r_lse, hbuf, part, top_lp, top_tok,
-      o_count, o_hyp, o_tok, o_pack, o_off, wh_t, kvs, anc, wkv_t, xbuf, attn_part, wout_t, total;
+      o_count, o_hyp, o_tok, o_pack, o_off, wh_t, kvs, anc, wkv_t, xbuf, attn_part, wout_t, wd3, w_exp, w_ln, w_li,
+      w_lv, wt_off, wt_col, wt_val, hd, s_hd, q_hd, haux, s_haux, q_haux, total;
 };
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+// The exact bf16 recurrence: its K loop takes 4 x 32 values per workgroup
+// pass and its digit sums stay exact in fp64 up to 2048 state values.
+bool rec_i8_eligible(const sb_model &m) { return m.dtype == SB_BF16 && m.d % 128 == 0 && m.d <= 2048; }
 
 int kbucket_of(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
 
@@ -129,6 +134,22 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
   if (m.attn) {
     L.xbuf = take(Rm * d * 2);
     L.attn_part = take(Rm * (size_t)m.kv_layers * d * 8);
+  }
+  if (rec_i8_eligible(m)) {
+    L.wd3 = take(3 * d * d);
+    L.w_exp = take(d * 4);
+    L.w_ln = take((d + 1) * 4);
+    L.w_li = take(d * REC_WLIST * 4);
+    L.w_lv = take(d * REC_WLIST * 4);
+    L.wt_off = take(d / 32 * 33 * 4);
+    L.wt_col = take(d / 32 * REC_WTILE * 4);
+    L.wt_val = take(d / 32 * REC_WTILE * 4);
+    L.hd = take(Rm * 3 * d);
+    L.s_hd = take(nk * 3 * d);
+    L.q_hd = take(Q * 3 * d);
+    L.haux = take(Rm * sizeof(RowAux));
+    L.s_haux = take(nk * sizeof(RowAux));
+    L.q_haux = take(Q * sizeof(RowAux));
   }
   L.total = off;
   return L;
@@ -390,6 +411,23 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   st.xbuf = model->attn ? w + L.xbuf : nullptr;
   st.attn_part = model->attn ? reinterpret_cast<double *>(w + L.attn_part) : nullptr;
   st.proj_in = model->attn ? st.xbuf : st.hbuf;
+  st.rec_i8 = 0;
+  if (rec_i8_eligible(*model)) {
+    st.wd3 = reinterpret_cast<int8_t *>(w + L.wd3);
+    st.w_exp = reinterpret_cast<int32_t *>(w + L.w_exp);
+    st.w_ln = reinterpret_cast<int32_t *>(w + L.w_ln);
+    st.w_li = reinterpret_cast<int32_t *>(w + L.w_li);
+    st.w_lv = reinterpret_cast<float *>(w + L.w_lv);
+    st.wt_off = reinterpret_cast<int32_t *>(w + L.wt_off);
+    st.wt_col = reinterpret_cast<int32_t *>(w + L.wt_col);
+    st.wt_val = reinterpret_cast<float *>(w + L.wt_val);
+    st.hd = reinterpret_cast<int8_t *>(w + L.hd);
+    st.s_hd = reinterpret_cast<int8_t *>(w + L.s_hd);
+    st.q_hd = reinterpret_cast<int8_t *>(w + L.q_hd);
+    st.haux = reinterpret_cast<RowAux *>(w + L.haux);
+    st.s_haux = reinterpret_cast<RowAux *>(w + L.s_haux);
+    st.q_haux = reinterpret_cast<RowAux *>(w + L.q_haux);
+  }
   st.W_h = model->W_h;
   st.E = model->E;
   st.W_out = model->W_out;
@@ -449,6 +487,16 @@ sb_status init_decoder(sb_decoder *dec, const sb_model *model, const sb_params *
   if (model->kv_layers > 0 &&
       launch_relayout_wkv(st, static_cast<const uint16_t *>(model->W_kv), dec->stream) != hipSuccess)
     return SB_E_HIP;
+  if (rec_i8_eligible(*model)) {
+    // W_h's digit planes; a W_h with more small values in a row or a tile
+    // than the lists hold keeps the fp64 recurrence.
+    int32_t overflow = 1;
+    if (launch_rec_prepare(st, dec->stream) != hipSuccess ||
+        hipMemcpyAsync(&overflow, st.w_ln + st.d, sizeof(int32_t), hipMemcpyDeviceToHost, dec->stream) != hipSuccess ||
+        hipStreamSynchronize(dec->stream) != hipSuccess)
+      return SB_E_HIP;
+    st.rec_i8 = overflow ? 0 : 1;
+  }
   return SB_OK;
 }
 
@@ -584,6 +632,9 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const int64_t *ids, const vo
   }
   HIPCHK(hipMemcpyAsync(static_cast<unsigned char *>(dec->st.q_h0) + q0 * rowbytes, h0, count * rowbytes,
                         hipMemcpyDeviceToDevice, dec->stream));
+  if (dec->st.rec_i8)
+    HIPCHK(launch_row_digits(dec->st, static_cast<unsigned char *>(dec->st.q_h0) + q0 * rowbytes, count,
+                             dec->st.q_hd + (size_t)q0 * 3 * dec->model.d, dec->st.q_haux + q0, dec->stream));
   HIPCHK(hipMemcpyAsync(dec->st.q_Lx + q0, lx, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
   HIPCHK(hipMemcpyAsync(dec->st.q_ml + q0, ml, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
   dec->n_queued += count;
@@ -783,6 +834,10 @@ sb_status sb_debug_expand(sb_decoder *dec, int32_t R, const void *h_prev, const 
   std::vector<int32_t> src(R);
   for (int r = 0; r < R; ++r) src[r] = r;   // states placed in slots 0..R-1
   HIPCHK(hipMemcpyAsync(st.s_h, h_prev, R * rowbytes, hipMemcpyDeviceToDevice, dec->stream));
+  if (st.rec_i8) {
+    HIPCHK(launch_row_digits(st, st.s_h, R, st.s_hd, st.s_haux, dec->stream));
+    HIPCHK(launch_aux_reset(st.haux, R, dec->stream));
+  }
   HIPCHK(hipMemcpyAsync(st.r_hsrc, src.data(), sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));
   HIPCHK(hipMemcpyAsync(st.r_y, y, sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));
   HIPCHK(hipMemcpyAsync(st.r_t, t, sizeof(int32_t) * R, hipMemcpyHostToDevice, dec->stream));

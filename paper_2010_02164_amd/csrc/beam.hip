@@ -645,6 +645,21 @@ __global__ __launch_bounds__(NT) void k_beam(DevState st) {
     const int r = x / chunks, c = x - r * chunks;
     if (nstat[r] == SLOT_ACTIVE) sh[(size_t)(base + r) * chunks + c] = hb[(size_t)sl_row[npar[r]] * chunks + c];
   }
+  // The state's digit planes and list, for the exact bf16 recurrence.
+  if (st.rec_i8) {
+    const int dch = 3 * st.d / 16, ach = (int)(sizeof(RowAux) / 16), tch = dch + ach;
+    const uint4 *__restrict__ hd = reinterpret_cast<const uint4 *>(st.hd);
+    uint4 *__restrict__ shd = reinterpret_cast<uint4 *>(st.s_hd);
+    const uint4 *__restrict__ ha = reinterpret_cast<const uint4 *>(st.haux);
+    uint4 *__restrict__ sha = reinterpret_cast<uint4 *>(st.s_haux);
+    for (int x = tid; x < w * tch; x += NT) {
+      const int r = x / tch, c = x - r * tch;
+      if (nstat[r] != SLOT_ACTIVE) continue;
+      const size_t src = sl_row[npar[r]];
+      if (c < dch) shd[(size_t)(base + r) * dch + c] = hd[src * dch + c];
+      else sha[(size_t)(base + r) * ach + (c - dch)] = ha[src * ach + (c - dch)];
+    }
+  }
   // KV state: an active child's ancestors are its parent's (levels 0 .. t-2)
   // and the parent itself (level t-1), copied into the other buffer as
   // 4-byte words; the word holding level t-1 is built by one thread.

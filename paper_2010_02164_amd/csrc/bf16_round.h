@@ -26,4 +26,19 @@ __device__ __forceinline__ uint16_t bf16_rne_from_double(double x) {
   return (uint16_t)(__float_as_uint(f) >> 16);
 }
 
+// bf16 of tanh(x) (nearest, ties to even) as if tanh were taken in fp64.
+// tanh is first taken in fp32: that value is within a few fp32 ulps of the
+// exact one (rounding x to fp32 adds at most one ulp, as
+// |x tanh'(x)| <= |tanh(x)|), so unless it lies within 64 ulps of a tie
+// between two bf16 values it rounds to the same bf16 as the exact value.
+// Near a tie, and for |x| < 2^-100, tanh is taken in fp64.
+__device__ __forceinline__ uint16_t bf16_tanh(double x) {
+  if (fabs(x) >= 0x1p-100) {
+    const uint32_t u = __float_as_uint(tanhf((float)x));
+    const uint32_t lo = u & 0xFFFFu;
+    if (lo < 0x8000u - 64u || lo > 0x8000u + 64u) return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+  }
+  return bf16_rne_from_double(tanh(x));
+}
+
 }  // namespace sb

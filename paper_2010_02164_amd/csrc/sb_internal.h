@@ -14,6 +14,18 @@ enum : int32_t { SLOT_EMPTY = 0, SLOT_ACTIVE = 1, SLOT_EOS = 2, SLOT_MAXLEN = 3 
 constexpr uint32_t BP_NOOP = 0xFFFFFFu;
 constexpr int KMAX_SUPPORTED = 16;
 
+// Exact bf16 recurrence: a state row's bf16 values, scaled by 2^(21 - F),
+// as three signed 7-bit digit planes (int8), plus the values of the row too
+// small for that window (|x| < 2^(F - 13)), kept as (column, value).
+constexpr int REC_HL = 15;
+struct RowAux {
+  int32_t F;                 // row exponent: every |x| < 2^F
+  int32_t n;                 // out-of-window values (> REC_HL: not all kept)
+  int32_t col[REC_HL];
+  float val[REC_HL];
+};
+static_assert(sizeof(RowAux) == 128, "RowAux is copied as 8 x 16 bytes");
+
 // Device-side control block: the scheduler state of Alg. 1 and the counters.
 struct DevCtrl {
   int32_t n_queued;   // inputs submitted so far
@@ -89,6 +101,22 @@ struct DevState {
   void *xbuf;
   double *attn_part;   // [R_max][L][d] per-layer read-outs a_l
   const void *proj_in; // rows the projection reads: xbuf (attn) or hbuf
+  // Exact bf16 recurrence (rec_i8 = 1, bf16 with d a multiple of 256): W_h
+  // as three signed 7-bit digit planes of W_h[o][i] * 2^(21 - w_exp[o]) in
+  // MFMA fragment order, per row the values outside that window, and state
+  // rows as digit planes [3][d] with their RowAux: the new states of the
+  // step (hd), the candidate slots (s_hd) and the queued encodings (q_hd).
+  int32_t rec_i8;
+  int8_t *wd3;         // [d/32][d/32][3 planes][64 lanes][16 bytes]
+  int32_t *w_exp;      // [d] smallest e with |W_h[o][i]| < 2^e
+  int32_t *w_ln;       // [d + 1] out-of-window values per row; [d]: 1 if a list overflowed
+  int32_t *w_li;       // [d][REC_WLIST] their columns
+  float *w_lv;         // [d][REC_WLIST] their values
+  int32_t *wt_off;     // [d/32][33] the lists of an output tile, concatenated: row starts
+  int32_t *wt_col;     // [d/32][REC_WTILE] columns (ascending within a row)
+  float *wt_val;       // [d/32][REC_WTILE] values
+  int8_t *hd, *s_hd, *q_hd;     // [rows][3][d]
+  RowAux *haux, *s_haux, *q_haux;
   // fp32 W_h in the recurrence's A-fragment order: [d/32][d/8][64 lanes][16 B],
   // lane (h, l) of output tile vt at K step s holding W_h[32 vt + l][8 s + 4h .. +3]
   // bf16 W_h likewise for the fp64 recurrence: [d/32][d/16][2 row halves][64 lanes][8 B],
@@ -118,6 +146,11 @@ struct DevState {
   float beta;
 };
 
+// Out-of-window values kept per W_h row by the exact bf16 recurrence, and
+// per tile of 32 rows; a W_h with more uses the fp64 recurrence.
+constexpr int REC_WLIST = 16;
+constexpr int REC_WTILE = 64;
+
 // Tile sizes of the projection/recurrence GEMMs.
 constexpr int GEMM_BV = 128;   // out features (vocab / hidden) per workgroup
 constexpr int GEMM_BR = 64;    // batch rows per workgroup
@@ -128,6 +161,9 @@ inline int proj_tiles(int V) { return (V + GEMM_BV - 1) / GEMM_BV; }
 hipError_t launch_sched(const DevState &st, hipStream_t s);
 hipError_t launch_rec(const DevState &st, hipStream_t s);
 hipError_t launch_relayout_wh(const DevState &st, hipStream_t s);
+hipError_t launch_rec_prepare(const DevState &st, hipStream_t s);
+hipError_t launch_row_digits(const DevState &st, const void *rows, int count, int8_t *dig, RowAux *aux, hipStream_t s);
+hipError_t launch_aux_reset(RowAux *aux, int count, hipStream_t s);
 hipError_t launch_proj(const DevState &st, hipStream_t s);
 hipError_t launch_rowmerge(const DevState &st, hipStream_t s);
 hipError_t launch_beam(const DevState &st, hipStream_t s);

@@ -377,6 +377,10 @@ __global__ __launch_bounds__(SCHED_THREADS) void k_sched(DevState st) {
           else y = st.s_tok[s];
           st.r_slot[row] = s;
           st.r_hsrc[row] = stp[u] == 0 ? -1 - inp[u] : s;   // a fresh beam reads its encoding h0
+          if (st.rec_i8) {
+            st.haux[row].F = 1;
+            st.haux[row].n = 0;
+          }
           st.r_y[row] = y;
           st.r_t[row] = stp[u] + 1;
           st.r_Lx[row] = lx;

@@ -1,5 +1,7 @@
 """Decoder-step kernels (recurrence, projection + log-sum-exp + per-row
 top-k, row merge) against the oracle's fp64 decoder on explicit rows."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -9,14 +11,16 @@ from synthgen import make_workload, scaled
 pytestmark = pytest.mark.gpu
 
 
-def _expand_case(wl, R, seed):
+def _expand_case(wl, R, seed, h_prev=None):
     import torch
     from paper_2010_02164_amd import decoder_for_workload
     rng = np.random.default_rng(seed)
     c = wl.cfg
     dec = decoder_for_workload(wl, max_inputs=4)
     R = min(R, c.n * c.k)
-    h_prev = np.tanh(rng.standard_normal((R, c.d))).astype(np.float32)
+    if h_prev is None:
+        h_prev = np.tanh(rng.standard_normal((R, c.d))).astype(np.float32)
+    R = h_prev.shape[0]
     if wl.is_bf16:
         from synthgen.gen import bf16_bits_to_f32, f32_to_bf16_bits
         h_prev = bf16_bits_to_f32(f32_to_bf16_bits(h_prev))
@@ -80,3 +84,72 @@ def test_expand_bf16(gpu, over):
     _, _, _, _, h_gpu, lse, lp, tok, h_ref, lp_ref = _expand_case(wl, 640 if over["V"] >= 32000 else 200, 12)
     print(f"[expand] bf16 {over}", flush=True)
     _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse)
+
+
+# The bf16 recurrence sums W_h h exactly from 7-bit digits of the values
+# scaled per W_h row and per state row, with the values too small for a
+# row's 21-bit window added from per-row lists (a state row whose list
+# overflows is scanned, a W_h whose lists overflow keeps the fp64 MFMA sum).
+# These cases put such values, zeros, signed zeros, subnormals and large
+# entries into W_h and the states; the states must stay bit-identical.
+def _bf16(x):
+    from synthgen.gen import bf16_bits_to_f32, f32_to_bf16_bits
+    return bf16_bits_to_f32(f32_to_bf16_bits(np.asarray(x, np.float32)))
+
+
+def _tiny(rng, cnt, lo=-40, hi=-16):
+    return rng.choice([-1.0, 1.0], cnt) * 2.0 ** rng.uniform(lo, hi, cnt)
+
+
+def _planted_wh(wl, rng, long_row=0):
+    d = wl.cfg.d
+    W = wl.W_h.copy()
+    for o, cnt in [(0, 1), (1, 5), (2, 12), (40, 3), (1000 % d, 8)]:
+        W[o, rng.choice(d, cnt, replace=False)] = _tiny(rng, cnt)
+    W[7, 3] = 0.9                      # a large entry widens the row's window
+    W[8, :5] = 1e-39                   # bf16 subnormals
+    W[9, 10:20] = 0.0
+    W[9, 20] = -0.0
+    if long_row:
+        W[5, rng.choice(d, long_row, replace=False)] = _tiny(rng, long_row)
+    return dataclasses.replace(wl, W_h=_bf16(W))
+
+
+def _planted_states(wl, rng, R):
+    d = wl.cfg.d
+    h = np.tanh(rng.standard_normal((R, d)))
+    for r, cnt in [(0, 3), (1, 40), (5, 15), (6, 16), (33, 2), (70, 100)]:
+        h[r, rng.choice(d, cnt, replace=False)] = _tiny(rng, cnt, -30, -14)
+    h[2] = 0.0
+    h[3, 0] = 6.0
+    h[4, :8] = 1e-39 * np.sign(rng.standard_normal(8))
+    h[4, 8:12] = -0.0
+    h[7] = _tiny(rng, d, -30, -20)     # a row of small values only
+    h[64:96] = 0.0                     # a whole tile of zero states
+    return _bf16(h)
+
+
+@pytest.mark.parametrize("long_row", [0, 40])
+def test_expand_bf16_small_values(gpu, long_row):
+    wl = _planted_wh(make_workload(scaled(4, N=4, V=8000, n=32)), np.random.default_rng(21), long_row)
+    h_prev = _planted_states(wl, np.random.default_rng(22), 200)
+    _, _, _, _, h_gpu, lse, lp, tok, h_ref, lp_ref = _expand_case(wl, 200, 23, h_prev=h_prev)
+    print(f"[expand] bf16 small values long_row={long_row}", flush=True)
+    _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse)
+
+
+def test_decode_bf16_small_values(gpu):
+    """Whole decodes with encodings holding small values, zeros and large
+    entries (their digits are made at submission) and the planted W_h."""
+    from tests.gpu_util import check_parity
+    rng = np.random.default_rng(31)
+    wl = _planted_wh(make_workload(scaled(4, N=24, V=8000, n=8)), rng)
+    h0 = wl.h0.copy()
+    for i, cnt in [(0, 3), (1, 40), (2, 15), (3, 16)]:
+        h0[i, rng.choice(wl.cfg.d, cnt, replace=False)] = _tiny(rng, cnt, -30, -12)
+    h0[4] = 0.0
+    h0[5, 0] = 60.0
+    h0[6, :8] = 1e-39
+    wl = dataclasses.replace(wl, h0=_bf16(h0))
+    print("[parity] bf16 small values", flush=True)
+    check_parity(wl, "var_stream")
