@@ -59,9 +59,10 @@ struct Layout {
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
-// The exact bf16 recurrence: its K loop takes 4 x 32 values per workgroup
-// pass and its digit sums stay exact in fp64 up to 2048 state values.
-bool rec_i8_eligible(const sb_model &m) { return m.dtype == SB_BF16 && m.d % 128 == 0 && m.d <= 2048; }
+// The exact bf16 recurrence: its K loop takes 4 waves x 2 blocks x 32
+// values per pass and its digit sums stay exact in fp64 up to 2048 state
+// values.
+bool rec_i8_eligible(const sb_model &m) { return m.dtype == SB_BF16 && m.d % 256 == 0 && m.d <= 2048; }
 
 int kbucket_of(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
 
@@ -144,9 +145,9 @@ Layout layout_of(const sb_model &m, const sb_params &p) {
     L.wt_off = take(d / 32 * 33 * 4);
     L.wt_col = take(d / 32 * REC_WTILE * 4);
     L.wt_val = take(d / 32 * REC_WTILE * 4);
-    L.hd = take(Rm * 3 * d);
-    L.s_hd = take(nk * 3 * d);
-    L.q_hd = take(Q * 3 * d);
+    L.hd = take(Rm * rec_dig_row_bytes(d));
+    L.s_hd = take(nk * rec_dig_row_bytes(d));
+    L.q_hd = take(Q * rec_dig_row_bytes(d));
     L.haux = take(Rm * sizeof(RowAux));
     L.s_haux = take(nk * sizeof(RowAux));
     L.q_haux = take(Q * sizeof(RowAux));
@@ -634,7 +635,7 @@ sb_status sb_submit(sb_decoder *dec, int32_t count, const int64_t *ids, const vo
                         hipMemcpyDeviceToDevice, dec->stream));
   if (dec->st.rec_i8)
     HIPCHK(launch_row_digits(dec->st, static_cast<unsigned char *>(dec->st.q_h0) + q0 * rowbytes, count,
-                             dec->st.q_hd + (size_t)q0 * 3 * dec->model.d, dec->st.q_haux + q0, dec->stream));
+                             dec->st.q_hd + (size_t)q0 * rec_dig_row_bytes(dec->model.d), dec->st.q_haux + q0, dec->stream));
   HIPCHK(hipMemcpyAsync(dec->st.q_Lx + q0, lx, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
   HIPCHK(hipMemcpyAsync(dec->st.q_ml + q0, ml, sizeof(int32_t) * count, hipMemcpyHostToDevice, dec->stream));
   dec->n_queued += count;

@@ -647,7 +647,7 @@ __global__ __launch_bounds__(NT) void k_beam(DevState st) {
   }
   // The state's digit planes and list, for the exact bf16 recurrence.
   if (st.rec_i8) {
-    const int dch = 3 * st.d / 16, ach = (int)(sizeof(RowAux) / 16), tch = dch + ach;
+    const int dch = (int)(rec_dig_row_bytes(st.d) / 16), ach = (int)(sizeof(RowAux) / 16), tch = dch + ach;
     const uint4 *__restrict__ hd = reinterpret_cast<const uint4 *>(st.hd);
     uint4 *__restrict__ shd = reinterpret_cast<uint4 *>(st.s_hd);
     const uint4 *__restrict__ ha = reinterpret_cast<const uint4 *>(st.haux);

@@ -174,10 +174,10 @@ __device__ __forceinline__ void emit_state_digits4(const DevState &st, int r, in
   bool in[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) in[q] = bf16_digits3(h[q], 1, dg[q][0], dg[q][1], dg[q][2]);
-  int8_t *dst = st.hd + (size_t)r * 3 * d + o;
+  int8_t *dst = st.hd + (size_t)r * rec_dig_row_bytes(d);
 #pragma unroll
   for (int p = 0; p < 3; ++p)
-    *reinterpret_cast<uint32_t *>(dst + (size_t)p * d) =
+    *reinterpret_cast<uint32_t *>(dst + rec_dig_off(o, p)) =
         (uint32_t)(uint8_t)dg[0][p] | ((uint32_t)(uint8_t)dg[1][p] << 8) | ((uint32_t)(uint8_t)dg[2][p] << 16) |
         ((uint32_t)(uint8_t)dg[3][p] << 24);
 #pragma unroll
@@ -272,7 +272,7 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
 // Digit planes and list of the state feeding row r.
 __device__ __forceinline__ const int8_t *row_digits(const DevState &st, int r) {
   const int src = st.r_hsrc[r];
-  return src >= 0 ? st.s_hd + (size_t)src * 3 * st.d : st.q_hd + (size_t)(-1 - src) * 3 * st.d;
+  return (src >= 0 ? st.s_hd : st.q_hd) + (size_t)(src >= 0 ? src : -1 - src) * rec_dig_row_bytes(st.d);
 }
 __device__ __forceinline__ const RowAux *row_aux(const DevState &st, int r) {
   const int src = st.r_hsrc[r];
@@ -285,7 +285,7 @@ __device__ __forceinline__ bool w_in_window(uint32_t b, int Ew) {
 }
 
 // The exact tile: 32 out features x 32 rows, the K range split over the
-// RSPLIT_I8 = 4 waves of a 256-thread workgroup (three fit on a compute
+// RSPLIT_I8 = 4 waves of a 256-thread workgroup (two fit on a compute
 // unit); the waves' T_s are added into LDS (integer sums, any order).
 // The out-of-window corrections are staged through LDS so that no chain of
 // dependent loads is left for the epilogue: the tile's W_h lists (built
@@ -324,7 +324,7 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
   const int v0 = vt * RT, r0 = rt * RT;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
-  const int kbw = d / RSPLIT_I8 / 32;         // K-blocks of 32 per wave
+  const int kbw = d / RSPLIT_I8 / 32;         // K-blocks of 32 per wave (even)
   const int kb0 = w * kbw;
   // Epilogue mapping: thread -> row j = tid/8, outputs v0 + 4*(tid%8) .. +3.
   const int j = tid >> 3, i0 = (tid & 7) * 4;
@@ -374,7 +374,7 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
   }
   // A: lane (h, l) holds the digits of W_h[v0 + l][32 kb + 16 h .. +15];
   // B likewise for state row r0 + l (K values in the same lane order).
-  const int8_t *bdig = row_digits(st, min(r0 + l32, R - 1)) + 16 * hh;
+  const int8_t *bdig = row_digits(st, min(r0 + l32, R - 1)) + 48 * hh;
   const u4 *ap = reinterpret_cast<const u4 *>(st.wd3) + ((size_t)vt * nkb + kb0) * 3 * 64 + lane;
   __syncthreads();
   // Gathers held in registers through the K loop (the rest after it).
@@ -389,19 +389,35 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
   v16i T[5];
 #pragma unroll
   for (int q = 0; q < 5; ++q) T[q] = v16i{};
-  for (int kb = 0; kb < kbw; ++kb) {
-    u4 A[3], B[3];
+  // Two K-blocks of operands in flight. Loads complete in issue order and
+  // every step issues the same loads (past the end, the last block again),
+  // so the wait before a block's MFMAs leaves the other block's loads
+  // outstanding; within a block the order follows first use.
+  u4 A[2][3], B[2][3];
+  auto load = [&](u4 *Ar, u4 *Br, int kb) {
+    Ar[0] = ap[(size_t)(kb * 3) * 64];
 #pragma unroll
-    for (int a = 0; a < 3; ++a) {
-      A[a] = ap[(size_t)(kb * 3 + a) * 64];
-      B[a] = *reinterpret_cast<const u4 *>(bdig + (size_t)a * d + (kb0 + kb) * 32);
+    for (int b = 0; b < 3; ++b) Br[b] = *reinterpret_cast<const u4 *>(bdig + (kb0 + kb) * 128 + b * 16);
+    Ar[1] = ap[(size_t)(kb * 3 + 1) * 64];
+    Ar[2] = ap[(size_t)(kb * 3 + 2) * 64];
+  };
+  load(A[0], B[0], 0);
+  __builtin_amdgcn_sched_barrier(0);
+  load(A[1], B[1], 1);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int kb = 0; kb < kbw; kb += 2) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b)
+          T[a + b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(v4i, A[s][a]),
+                                                           __builtin_bit_cast(v4i, B[s][b]), T[a + b], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      load(A[s], B[s], min(kb + s + 2, kbw - 1));
+      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int a = 0; a < 3; ++a)
-#pragma unroll
-      for (int b = 0; b < 3; ++b)
-        T[a + b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(v4i, A[a]), __builtin_bit_cast(v4i, B[b]),
-                                                         T[a + b], 0, 0, 0);
   }
 #pragma unroll
   for (int g = 0; g < REC_GATHER; ++g) {
@@ -478,7 +494,7 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
 }
 
 // Persistent exact bf16 recurrence over the active tiles (RecWalk).
-__global__ __launch_bounds__(RTHREADS_I8, 3) void k_rec_i8(DevState st) {
+__global__ __launch_bounds__(RTHREADS_I8, 2) void k_rec_i8(DevState st) {
   const int R = st.ctrl->R;
   if (R <= 0) return;
   const RecWalk walk(st.d / RT, (R + RT - 1) / RT, blockIdx.x & 7);
@@ -509,7 +525,7 @@ __global__ __launch_bounds__(256) void k_row_digits(const uint16_t *__restrict__
   atomicMax(&smx, bf16_max_eu(x, threadIdx.x, d, blockDim.x));
   __syncthreads();
   const int E = smx - 126;
-  int8_t *dr = dig + (size_t)r * 3 * d;
+  int8_t *dr = dig + (size_t)r * rec_dig_row_bytes(d);
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     int a0, a1, a2;
     if (!bf16_digits3(x[i], E, a0, a1, a2)) {
@@ -519,9 +535,9 @@ __global__ __launch_bounds__(256) void k_row_digits(const uint16_t *__restrict__
         aux[r].val[k] = bf16f(x[i]);
       }
     }
-    dr[i] = (int8_t)a0;
-    dr[d + i] = (int8_t)a1;
-    dr[2 * d + i] = (int8_t)a2;
+    dr[rec_dig_off(i, 0)] = (int8_t)a0;
+    dr[rec_dig_off(i, 1)] = (int8_t)a1;
+    dr[rec_dig_off(i, 2)] = (int8_t)a2;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -706,7 +722,7 @@ hipError_t launch_rec(const DevState &st, hipStream_t s) {
   // bf16 (66 KB of LDS each), four for fp32 (33 KB).
   const int tiles = xcd_grid((st.d / RT) * ((st.R_max + RT - 1) / RT));
   if (st.rec_i8) {
-    const int G = std::max(8, std::min(st.n_cu * 3 / 8 * 8, tiles));
+    const int G = std::max(8, std::min(st.n_cu * 2 / 8 * 8, tiles));
     hipLaunchKernelGGL(k_rec_i8, dim3(G), dim3(RTHREADS_I8), 0, s, st);
     return hipGetLastError();
   }

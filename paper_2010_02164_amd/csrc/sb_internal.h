@@ -101,10 +101,10 @@ struct DevState {
   void *xbuf;
   double *attn_part;   // [R_max][L][d] per-layer read-outs a_l
   const void *proj_in; // rows the projection reads: xbuf (attn) or hbuf
-  // Exact bf16 recurrence (rec_i8 = 1, bf16 with d a multiple of 256): W_h
+  // Exact bf16 recurrence (rec_i8 = 1, bf16, d a multiple of 256, <= 2048): W_h
   // as three signed 7-bit digit planes of W_h[o][i] * 2^(21 - w_exp[o]) in
   // MFMA fragment order, per row the values outside that window, and state
-  // rows as digit planes [3][d] with their RowAux: the new states of the
+  // rows as digit planes (rec_dig_off) with their RowAux: the new states of the
   // step (hd), the candidate slots (s_hd) and the queued encodings (q_hd).
   int32_t rec_i8;
   int8_t *wd3;         // [d/32][d/32][3 planes][64 lanes][16 bytes]
@@ -115,7 +115,7 @@ struct DevState {
   int32_t *wt_off;     // [d/32][33] the lists of an output tile, concatenated: row starts
   int32_t *wt_col;     // [d/32][REC_WTILE] columns (ascending within a row)
   float *wt_val;       // [d/32][REC_WTILE] values
-  int8_t *hd, *s_hd, *q_hd;     // [rows][3][d]
+  int8_t *hd, *s_hd, *q_hd;     // [rows][4d bytes]: digit (k, a) at rec_dig_off(k, a)
   RowAux *haux, *s_haux, *q_haux;
   // fp32 W_h in the recurrence's A-fragment order: [d/32][d/8][64 lanes][16 B],
   // lane (h, l) of output tile vt at K step s holding W_h[32 vt + l][8 s + 4h .. +3]
@@ -150,6 +150,13 @@ struct DevState {
 // per tile of 32 rows; a W_h with more uses the fp64 recurrence.
 constexpr int REC_WLIST = 16;
 constexpr int REC_WTILE = 64;
+
+// A state row's digit planes, 128 bytes per 32 values: for value k and
+// plane a, byte 48 ((k / 16) % 2) + 16 a + k % 16 of block k / 32 (the last
+// 32 bytes of a block unused), so that one lane's three 16-byte MFMA
+// operands lie together and a block is one 128-byte line.
+__host__ __device__ constexpr int rec_dig_off(int k, int a) { return (k >> 5) * 128 + ((k >> 4) & 1) * 48 + a * 16 + (k & 15); }
+constexpr size_t rec_dig_row_bytes(size_t d) { return 4 * d; }
 
 // Tile sizes of the projection/recurrence GEMMs.
 constexpr int GEMM_BV = 128;   // out features (vocab / hidden) per workgroup
