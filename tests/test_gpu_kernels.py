@@ -138,12 +138,14 @@ def test_expand_bf16_small_values(gpu, long_row):
     _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse)
 
 
-def test_decode_bf16_small_values(gpu):
+@pytest.mark.parametrize("long_row", [0, 40])
+def test_decode_bf16_small_values(gpu, long_row):
     """Whole decodes with encodings holding small values, zeros and large
-    entries (their digits are made at submission) and the planted W_h."""
+    entries (their digits are made at submission) and the planted W_h (with
+    a 40-value row list: the whole decode on the fp64 recurrence)."""
     from tests.gpu_util import check_parity
     rng = np.random.default_rng(31)
-    wl = _planted_wh(make_workload(scaled(4, N=24, V=8000, n=8)), rng)
+    wl = _planted_wh(make_workload(scaled(4, N=24, V=8000, n=8)), rng, long_row)
     h0 = wl.h0.copy()
     for i, cnt in [(0, 3), (1, 40), (2, 15), (3, 16)]:
         h0[i, rng.choice(wl.cfg.d, cnt, replace=False)] = _tiny(rng, cnt, -30, -12)
@@ -151,5 +153,5 @@ def test_decode_bf16_small_values(gpu):
     h0[5, 0] = 60.0
     h0[6, :8] = 1e-39
     wl = dataclasses.replace(wl, h0=_bf16(h0))
-    print("[parity] bf16 small values", flush=True)
+    print(f"[parity] bf16 small values long_row={long_row}", flush=True)
     check_parity(wl, "var_stream")

@@ -31,6 +31,8 @@ def _run(wl, sched, noalloc):
 @pytest.mark.parametrize("order", ["large_then_small"])
 def test_noalloc_matches_sb_create(gpu, order):
     cases = [
+        # bf16 with the exact recurrence's digit buffers and short tile lists, ~12 MiB
+        (make_workload(scaled(4, N=48, n=8, V=8320, d=512)), "var_stream"),
         (make_workload(scaled(2, N=1024, n=64)), "var_stream"),   # ~10 MiB of workspace
         (make_workload(scaled(1, N=24, n=4)), "var_fifo"),        # smaller, over the same scratch
     ]
@@ -40,7 +42,8 @@ def test_noalloc_matches_sb_create(gpu, order):
         assert got == ref                     # same kernels, same arithmetic: bit for bit
         assert st_got == st_ref and hist_got == hist_ref
         o = decode_workload(wl, sched=sched)
-        rep = compare(o.hyps, o.min_margin, [[(t, s, u) for t, s, u, _ in y] for y in got])
+        rep = compare(o.hyps, o.min_margin, [[(t, s, u) for t, s, u, _ in y] for y in got],
+                      score_tol=2e-2 if wl.is_bf16 else 1e-4)
         print(f"[noalloc] {wl.cfg.name} {sched} N={len(wl.Lx)}: {rep.summary()}", flush=True)
         assert rep.ok and rep.n_excused == 0, rep.failures[:3]
         assert st_got["expansions"] == o.expansions and st_got["timesteps"] == o.timesteps
