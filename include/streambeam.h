@@ -81,8 +81,11 @@ typedef enum { SB_RULE_PAPER = 0, SB_RULE_FAIRSEQ = 1 } sb_rule;
 
 /* Storage type of weights, h0 and decoder states. SB_F32: fp32 everywhere
  * (MFMA fp32, fp32 accumulation). SB_BF16: bf16 weights and states; the
- * projection accumulates in fp32, the recurrence pre-activation in fp64
- * (exact for bf16 products) so that the rounded bf16 state is reproducible. */
+ * projection accumulates in fp32; the recurrence pre-activation is the
+ * exact sum of the bf16 products (integer digit products, d a multiple of
+ * 256 up to 2048; otherwise, or when W_h has many values far below its
+ * rows' largest, an fp64 sum), rounded once to fp64, so that the rounded
+ * bf16 state is reproducible. h0 values must be finite. */
 typedef enum { SB_F32 = 0, SB_BF16 = 1 } sb_dtype;
 
 /* Status of a finalized hypothesis. */
