@@ -369,7 +369,7 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
   } else if (tid >= 64 && tid < 64 + RT + 1) {
     L.woff[tid - 64] = st.wt_off[vt * (RT + 1) + tid - 64];
   } else if (tid >= 128 && tid < 128 + REC_WTILE) {
-    L.wcol[tid - 128] = st.wt_col[vt * REC_WTILE + tid - 128];
+    L.wcol[tid - 128] = st.wt_col[vt * REC_WTILE + tid - 128] & 0xFFFF;
     L.wval[tid - 128] = st.wt_val[vt * REC_WTILE + tid - 128];
   }
   // A: lane (h, l) holds the digits of W_h[v0 + l][32 kb + 16 h .. +15];
@@ -493,18 +493,244 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
   emit_state_digits4(st, row, v0 + i0, hb);
 }
 
-// Persistent exact bf16 recurrence over the active tiles (RecWalk).
+// Epilogue of a wave's 32 x 32 quadrant (lane (h, l): row `row`, outputs
+// v0 + 8g + 4h + i at register 4g + i). Values below the windows: the
+// output tile's W_h list (sorted by output, then column) is held one entry
+// per lane and walked by the wave, each entry's state value gathered by the
+// lanes holding its output; a row's own list is walked by its lanes in
+// column order, or the row is scanned if the list overflowed. The fp64
+// corrections are thus added in a fixed order.
+__device__ __forceinline__ void rec_quadrant_epilogue(const DevState &st, const v16i *T, int v0, int row, int R,
+                                                      int src, int y, const RowAux *ax, int F, int hn, int ne,
+                                                      int wcol, float wval) {
+  const int d = st.d;
+  const int lane = threadIdx.x & 63, hh = lane >> 5;
+  int ew[16];
+  uint2 ev[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int o = v0 + 8 * g + 4 * hh;
+    const int4 e4 = *reinterpret_cast<const int4 *>(st.w_exp + o);
+    ew[4 * g] = e4.x;
+    ew[4 * g + 1] = e4.y;
+    ew[4 * g + 2] = e4.z;
+    ew[4 * g + 3] = e4.w;
+    ev[g] = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(st.E) + (size_t)y * d + o);
+  }
+  // Z = sum_s 128^s T_s (Horner, exact), scaled by 2^(E_w + F - 42).
+  double pre[16];
+#pragma unroll
+  for (int reg = 0; reg < 16; ++reg) {
+    double Z = (double)T[4][reg];
+#pragma unroll
+    for (int s2 = 3; s2 >= 0; --s2) Z = fma(Z, 128.0, (double)T[s2][reg]);
+    pre[reg] = ldexp(Z, ew[reg] + F - 42);
+  }
+  const uint16_t *hrow = src_row16(st, src);
+  // Entry e (held by lane e) of output f belongs to the lanes with
+  // h = (f / 4) % 2, at register 4 (f / 8) + f % 4.
+  for (int e0 = 0; e0 < ne; e0 += 16) {
+    uint16_t gv[16];
+#pragma unroll
+    for (int x = 0; x < 16; ++x) {
+      const int ce = __shfl(wcol, (e0 + x) & 63);
+      gv[x] = (e0 + x < ne && ((ce >> 18) & 1) == hh) ? hrow[ce & 0xFFFF] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int x = 0; x < 16; ++x) {
+      if (e0 + x >= ne) break;
+      const int ce = __builtin_amdgcn_readfirstlane(__shfl(wcol, e0 + x));
+      const float ve = __shfl(wval, e0 + x);
+      const int fe = ce >> 16, rege = 4 * (fe >> 3) + (fe & 3);
+      if (((fe >> 2) & 1) == hh) {
+#pragma unroll
+        for (int reg = 0; reg < 16; ++reg)
+          if (reg == rege) pre[reg] += (double)ve * (double)bf16f(gv[x]);
+      }
+    }
+  }
+  const uint16_t *Wh = static_cast<const uint16_t *>(st.W_h) + (size_t)(v0 + 4 * hh) * d;
+  auto add_h = [&](int col, double hv) {
+    uint16_t wb[16];
+#pragma unroll
+    for (int reg = 0; reg < 16; ++reg) wb[reg] = Wh[(size_t)(8 * (reg >> 2) + (reg & 3)) * d + col];
+#pragma unroll
+    for (int reg = 0; reg < 16; ++reg)
+      if (w_in_window(wb[reg], ew[reg])) pre[reg] += (double)bf16f(wb[reg]) * hv;
+  };
+  if (row >= R) return;
+  if (hn <= REC_HL) {
+    int last = -1;
+    for (int x = 0; x < hn; ++x) {   // next column after `last`
+      int c = d, k = 0;
+      for (int z = 0; z < hn; ++z) {
+        const int cz = ax->col[z];
+        if (cz > last && cz < c) {
+          c = cz;
+          k = z;
+        }
+      }
+      add_h(c, (double)ax->val[k]);
+      last = c;
+    }
+  } else {
+    for (int col = 0; col < d; ++col) {
+      const uint32_t hb = hrow[col];
+      if (!w_in_window(hb, F)) add_h(col, (double)bf16f((uint16_t)hb));
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    uint16_t hb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t e = (i & 2) ? ev[g].y : ev[g].x;
+      hb[i] = bf16_tanh(pre[4 * g + i] + (double)bf16f((uint16_t)((i & 1) ? e >> 16 : e & 0xFFFFu)));
+    }
+    const int o = v0 + 8 * g + 4 * hh;
+    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(st.hbuf) + (size_t)row * d + o) =
+        uint2{(uint32_t)hb[0] | ((uint32_t)hb[1] << 16), (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
+    emit_state_digits4(st, row, o, hb);
+  }
+}
+
+// Large steps: 64 out features x 64 rows per workgroup, each wave one
+// 32 x 32 quadrant over the whole K range, so a K-block's operands (64 W_h
+// rows and 64 state rows, 12 KB of digits) are fetched once for four
+// quadrants: half the bytes per output of the 32 x 32 tiles. The block
+// passes through a three-stage LDS ring (one barrier per block) and
+// R64_INFLIGHT more blocks are in flight in registers. Lane (h, l) of wave w ends with T_s for
+// row r0 + 32 (w / 2) + l and outputs v0 + 32 (w % 2) + 8g + 4h + i.
+constexpr int R64_STAGES = 3;
+constexpr int R64_INFLIGHT = 2;   // K-blocks in flight in registers (d / 32 a multiple of it)
+constexpr int R64_PIECES = 768;   // 16-byte pieces per K-block: 384 of W_h digits, 384 of state digits
+
+struct Rec64Lds {
+  u4 stage[R64_STAGES][R64_PIECES];
+};
+
+__device__ __forceinline__ void rec_tile64_i8(const DevState &st, Rec64Lds &L, int vq, int rq, int R) {
+  const int d = st.d, nkb = d / 32;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int fq = w & 1, rq4 = w >> 1;
+  const int vt = 2 * vq + fq, v0 = vt * RT;
+  const int r0 = 2 * rq * RT + rq4 * RT;
+  // The thread's three pieces of every K-block: piece p < 384 is W_h digit
+  // fragment p of output tiles 2vq, 2vq + 1 (the layout of wd3); piece
+  // 384 + q is the state fragment q: half q / 192 of the rows, plane
+  // (q / 64) % 3, lane q % 64 (row l, bytes 48h + 16 plane of the block).
+  const u4 *gp[3];
+  int gs[3];
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    const int p = tid + RTHREADS_I8 * i;
+    if (p < 384) {
+      const int f = p / 192, rem = p - 192 * f;
+      gp[i] = reinterpret_cast<const u4 *>(st.wd3) + (size_t)(2 * vq + f) * nkb * 192 + rem;
+      gs[i] = 192;
+    } else {
+      const int q = p - 384, hq = q / 192, rem = q - 192 * hq, a = rem / 64, ln = rem & 63;
+      const int src = st.r_hsrc[min(2 * rq * RT + hq * RT + (ln & 31), R - 1)];
+      gp[i] = reinterpret_cast<const u4 *>((src >= 0 ? st.s_hd : st.q_hd) +
+                                           (size_t)(src >= 0 ? src : -1 - src) * rec_dig_row_bytes(d) +
+                                           48 * (ln >> 5) + 16 * a);
+      gs[i] = 8;
+    }
+  }
+  // Epilogue inputs, fetched before the K loop.
+  const int row = r0 + l32, rowc = min(row, R - 1);
+  const int src = st.r_hsrc[rowc];
+  const int y = st.r_y[rowc];
+  const RowAux *ax = src >= 0 ? st.s_haux + src : st.q_haux + (-1 - src);
+  const int ne = st.wt_off[vt * (RT + 1) + RT];
+  const int wcol = lane < ne ? st.wt_col[vt * REC_WTILE + lane] : 0;
+  const float wval = lane < ne ? st.wt_val[vt * REC_WTILE + lane] : 0.0f;
+  const int F = ax->F, hn = ax->n;
+
+  u4 G[R64_INFLIGHT][3];
+  auto gload = [&](u4 *g, int kb) {
+#pragma unroll
+    for (int i = 0; i < 3; ++i) g[i] = gp[i][(size_t)kb * gs[i]];
+  };
+  auto lstore = [&](int sg, const u4 *g) {
+#pragma unroll
+    for (int i = 0; i < 3; ++i) L.stage[sg][tid + RTHREADS_I8 * i] = g[i];
+  };
+  v16i T[5];
+#pragma unroll
+  for (int q = 0; q < 5; ++q) T[q] = v16i{};
+  auto compute = [&](int sg) {
+    const u4 *stg = L.stage[sg];
+    u4 A[3], B[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      A[a] = stg[fq * 192 + a * 64 + lane];
+      B[a] = stg[384 + rq4 * 192 + a * 64 + lane];
+    }
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+      for (int b = 0; b < 3; ++b)
+        T[a + b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(v4i, A[a]), __builtin_bit_cast(v4i, B[b]),
+                                                         T[a + b], 0, 0, 0);
+  };
+  // Blocks 0 and 1 in stages 0 and 1, blocks 2 .. R64_INFLIGHT + 1 in
+  // flight. Step j reads stage j % 3, then stores block j + 2 into stage
+  // (j + 2) % 3 (last read at step j - 1, before the barrier that ended it)
+  // and fetches block j + 2 + R64_INFLIGHT; past the end the last block is
+  // fetched and stored again into a stage no later step reads, so every
+  // step issues the same loads.
+  gload(G[0], 0);
+  gload(G[1], 1);
+  lstore(0, G[0]);
+  lstore(1, G[1]);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int j = 0; j < R64_INFLIGHT; ++j) gload(G[j], min(2 + j, nkb - 1));
+  __syncthreads();
+  for (int kb = 0; kb < nkb; kb += R64_INFLIGHT) {
+#pragma unroll
+    for (int j = 0; j < R64_INFLIGHT; ++j) {
+      compute((kb + j) % R64_STAGES);
+      lstore((kb + j + 2) % R64_STAGES, G[j]);
+      __builtin_amdgcn_sched_barrier(0);
+      gload(G[j], min(kb + j + 2 + R64_INFLIGHT, nkb - 1));
+      __syncthreads();
+    }
+  }
+  rec_quadrant_epilogue(st, T, v0, row, R, src, y, ax, F, hn, ne, wcol, wval);
+}
+
+// Persistent exact bf16 recurrence over the active tiles (RecWalk): 64 x 64
+// tiles for steps with enough rows to fill half the grid with them, else
+// 32 x 32 tiles with the K range split over the waves.
 __global__ __launch_bounds__(RTHREADS_I8, 2) void k_rec_i8(DevState st) {
   const int R = st.ctrl->R;
   if (R <= 0) return;
+  __shared__ union {
+    RecI8Lds ks;
+    Rec64Lds t64;
+  } L;
+  const int nq = (R + 2 * RT - 1) / (2 * RT), nvq = st.d / (2 * RT);
+  if (nq * nvq * 2 >= (int)gridDim.x) {
+    // 64 x 64 tiles once they fill half the grid
+    const RecWalk walk(nvq, nq, blockIdx.x & 7);
+    for (int t = (int)(blockIdx.x >> 3); t < walk.n; t += (int)(gridDim.x >> 3)) {
+      int vq, rq;
+      walk.at(t, vq, rq);
+      rec_tile64_i8(st, L.t64, vq, rq, R);
+      __syncthreads();   // the ring is reused by the next tile
+    }
+    return;
+  }
   const RecWalk walk(st.d / RT, (R + RT - 1) / RT, blockIdx.x & 7);
-  __shared__ RecI8Lds L;
-  for (int i = threadIdx.x; i < 5 * RT * RS; i += RTHREADS_I8) (&L.redi[0][0])[i] = 0;
+  for (int i = threadIdx.x; i < 5 * RT * RS; i += RTHREADS_I8) (&L.ks.redi[0][0])[i] = 0;
   __syncthreads();
   for (int t = (int)(blockIdx.x >> 3); t < walk.n; t += (int)(gridDim.x >> 3)) {
     int vt, rt;
     walk.at(t, vt, rt);
-    rec_tile_i8(st, L, vt, rt, R);
+    rec_tile_i8(st, L.ks, vt, rt, R);
     __syncthreads();   // L is reused by the next tile
   }
 }
@@ -601,7 +827,8 @@ __global__ void k_w_digits(DevState st) {
 }
 
 // ... and, per output tile, the rows' lists sorted by column and
-// concatenated (one thread per row); w_ln[d] = 1 if a list overflowed.
+// concatenated (one thread per row), each entry's column with its row in
+// the tile above bit 16; w_ln[d] = 1 if a list overflowed.
 __global__ void k_w_tiles(DevState st) {
   const int vt = blockIdx.x, o = threadIdx.x;   // 32 threads
   const int n = st.w_ln[vt * RT + o];
@@ -635,7 +862,7 @@ __global__ void k_w_tiles(DevState st) {
       val[y - 1] = v;
     }
   for (int x = 0; x < m; ++x) {
-    st.wt_col[vt * REC_WTILE + off[o] + x] = col[x];
+    st.wt_col[vt * REC_WTILE + off[o] + x] = col[x] | (o << 16);
     st.wt_val[vt * REC_WTILE + off[o] + x] = val[x];
   }
 }

@@ -126,15 +126,21 @@ def _planted_states(wl, rng, R):
     h[4, 8:12] = -0.0
     h[7] = _tiny(rng, d, -30, -20)     # a row of small values only
     h[64:96] = 0.0                     # a whole tile of zero states
+    if R > 1000:
+        for r, cnt in [(700, 5), (701, 30), (1090, 15), (1099, 16)]:
+            h[r, rng.choice(d, cnt, replace=False)] = _tiny(rng, cnt, -30, -14)
+        h[1024:1088] = 0.0             # a whole 64-row tile of zero states
     return _bf16(h)
 
 
-@pytest.mark.parametrize("long_row", [0, 40])
-def test_expand_bf16_small_values(gpu, long_row):
-    wl = _planted_wh(make_workload(scaled(4, N=4, V=8000, n=32)), np.random.default_rng(21), long_row)
-    h_prev = _planted_states(wl, np.random.default_rng(22), 200)
-    _, _, _, _, h_gpu, lse, lp, tok, h_ref, lp_ref = _expand_case(wl, 200, 23, h_prev=h_prev)
-    print(f"[expand] bf16 small values long_row={long_row}", flush=True)
+@pytest.mark.parametrize("long_row,R", [(0, 200), (40, 200), (0, 1100)])
+def test_expand_bf16_small_values(gpu, long_row, R):
+    # 1 100 rows run the 64 x 64 tiles (a step whose 64-row tiles fill half
+    # the grid), 200 the 32 x 32 tiles with the K range split over waves.
+    wl = _planted_wh(make_workload(scaled(4, N=4, V=8000, n=128)), np.random.default_rng(21), long_row)
+    h_prev = _planted_states(wl, np.random.default_rng(22), R)
+    _, _, _, _, h_gpu, lse, lp, tok, h_ref, lp_ref = _expand_case(wl, R, 23, h_prev=h_prev)
+    print(f"[expand] bf16 small values long_row={long_row} R={R}", flush=True)
     _check_rows(wl, h_gpu, lp, tok, h_ref, lp_ref, lse)
 
 
