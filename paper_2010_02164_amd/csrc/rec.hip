@@ -269,6 +269,25 @@ __device__ __forceinline__ void rec_tile_bf16(const DevState &st, double (*red)[
   }
 }
 
+// A row's list record in registers (32 dwords: F, n, columns, values),
+// fetched with eight 16-byte loads at once.
+struct AuxRegs {
+  uint32_t w[32];
+};
+__device__ __forceinline__ AuxRegs load_aux(const RowAux *ax) {
+  AuxRegs r;
+  const u4 *p = reinterpret_cast<const u4 *>(ax);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const u4 v = p[i];
+    r.w[4 * i] = v.x;
+    r.w[4 * i + 1] = v.y;
+    r.w[4 * i + 2] = v.z;
+    r.w[4 * i + 3] = v.w;
+  }
+  return r;
+}
+
 // Digit planes and list of the state feeding row r.
 __device__ __forceinline__ const int8_t *row_digits(const DevState &st, int r) {
   const int src = st.r_hsrc[r];
@@ -337,10 +356,10 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
                                                     (size_t)st.r_y[min(row, R - 1)] * d + v0 + i0);
   if (tid < RT) {
     const int src = st.r_hsrc[min(r0 + tid, R - 1)];
-    const RowAux *ax = src >= 0 ? st.s_haux + src : st.q_haux + (-1 - src);
-    const int n = r0 + tid < R ? ax->n : 0;
+    const AuxRegs ar = load_aux(src >= 0 ? st.s_haux + src : st.q_haux + (-1 - src));
+    const int n = r0 + tid < R ? (int)ar.w[1] : 0;
     L.src[tid] = src;
-    L.F[tid] = ax->F;
+    L.F[tid] = (int)ar.w[0];
     int cnt = n > REC_HL ? 0 : n;
     int inc = cnt;   // inclusive scan over the 32 rows
 #pragma unroll
@@ -355,16 +374,19 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
     L.hcnt[tid] = cnt;
     L.scan[tid] = scan ? 1 : 0;
     if (tid == RT - 1) L.htot = min(inc, REC_HTILE);
-    for (int x = 0; x < cnt; ++x) {   // insertion into column order
-      const int c = ax->col[x];
-      const float v = ax->val[x];
-      int y = off + x;
-      for (; y > off && L.hcol[y - 1] > c; --y) {
-        L.hcol[y] = L.hcol[y - 1];
-        L.hval[y] = L.hval[y - 1];
+#pragma unroll
+    for (int x = 0; x < REC_HL; ++x) {   // insertion into column order
+      if (x < cnt) {
+        const int c = (int)ar.w[2 + x];
+        const float v = __uint_as_float(ar.w[2 + REC_HL + x]);
+        int y = off + x;
+        for (; y > off && L.hcol[y - 1] > c; --y) {
+          L.hcol[y] = L.hcol[y - 1];
+          L.hval[y] = L.hval[y - 1];
+        }
+        L.hcol[y] = c;
+        L.hval[y] = v;
       }
-      L.hcol[y] = c;
-      L.hval[y] = v;
     }
   } else if (tid >= 64 && tid < 64 + RT + 1) {
     L.woff[tid - 64] = st.wt_off[vt * (RT + 1) + tid - 64];
@@ -501,22 +523,20 @@ __device__ __forceinline__ void rec_tile_i8(const DevState &st, RecI8Lds &L, int
 // column order, or the row is scanned if the list overflowed. The fp64
 // corrections are thus added in a fixed order.
 __device__ __forceinline__ void rec_quadrant_epilogue(const DevState &st, const v16i *T, int v0, int row, int R,
-                                                      int src, int y, const RowAux *ax, int F, int hn, int ne,
-                                                      int wcol, float wval) {
+                                                      int src, const RowAux *ax, const int4 *ew4, const uint2 *ev,
+                                                      int ne, int wcol, float wval) {
   const int d = st.d;
   const int lane = threadIdx.x & 63, hh = lane >> 5;
+  const AuxRegs ar = load_aux(ax);   // in flight with the gathers below
   int ew[16];
-  uint2 ev[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const int o = v0 + 8 * g + 4 * hh;
-    const int4 e4 = *reinterpret_cast<const int4 *>(st.w_exp + o);
-    ew[4 * g] = e4.x;
-    ew[4 * g + 1] = e4.y;
-    ew[4 * g + 2] = e4.z;
-    ew[4 * g + 3] = e4.w;
-    ev[g] = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(st.E) + (size_t)y * d + o);
+    ew[4 * g] = ew4[g].x;
+    ew[4 * g + 1] = ew4[g].y;
+    ew[4 * g + 2] = ew4[g].z;
+    ew[4 * g + 3] = ew4[g].w;
   }
+  const uint16_t *hrow = src_row16(st, src);
   // Z = sum_s 128^s T_s (Horner, exact), scaled by 2^(E_w + F - 42).
   double pre[16];
 #pragma unroll
@@ -524,9 +544,11 @@ __device__ __forceinline__ void rec_quadrant_epilogue(const DevState &st, const 
     double Z = (double)T[4][reg];
 #pragma unroll
     for (int s2 = 3; s2 >= 0; --s2) Z = fma(Z, 128.0, (double)T[s2][reg]);
-    pre[reg] = ldexp(Z, ew[reg] + F - 42);
+    pre[reg] = Z;
   }
-  const uint16_t *hrow = src_row16(st, src);
+  const int F = (int)ar.w[0], hn = (int)ar.w[1];
+#pragma unroll
+  for (int reg = 0; reg < 16; ++reg) pre[reg] = ldexp(pre[reg], ew[reg] + F - 42);
   // Entry e (held by lane e) of output f belongs to the lanes with
   // h = (f / 4) % 2, at register 4 (f / 8) + f % 4.
   for (int e0 = 0; e0 < ne; e0 += 16) {
@@ -562,15 +584,17 @@ __device__ __forceinline__ void rec_quadrant_epilogue(const DevState &st, const 
   if (hn <= REC_HL) {
     int last = -1;
     for (int x = 0; x < hn; ++x) {   // next column after `last`
-      int c = d, k = 0;
-      for (int z = 0; z < hn; ++z) {
-        const int cz = ax->col[z];
-        if (cz > last && cz < c) {
+      int c = d;
+      uint32_t vb = 0u;
+#pragma unroll
+      for (int z = 0; z < REC_HL; ++z) {
+        const int cz = (int)ar.w[2 + z];
+        if (z < hn && cz > last && cz < c) {
           c = cz;
-          k = z;
+          vb = ar.w[2 + REC_HL + z];
         }
       }
-      add_h(c, (double)ax->val[k]);
+      add_h(c, (double)__uint_as_float(vb));
       last = c;
     }
   } else {
@@ -646,7 +670,14 @@ __device__ __forceinline__ void rec_tile64_i8(const DevState &st, Rec64Lds &L, i
   const int ne = st.wt_off[vt * (RT + 1) + RT];
   const int wcol = lane < ne ? st.wt_col[vt * REC_WTILE + lane] : 0;
   const float wval = lane < ne ? st.wt_val[vt * REC_WTILE + lane] : 0.0f;
-  const int F = ax->F, hn = ax->n;
+  int4 ew4[4];
+  uint2 ev[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int o = v0 + 8 * g + 4 * hh;
+    ew4[g] = *reinterpret_cast<const int4 *>(st.w_exp + o);
+    ev[g] = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(st.E) + (size_t)y * d + o);
+  }
 
   u4 G[R64_INFLIGHT][3];
   auto gload = [&](u4 *g, int kb) {
@@ -699,7 +730,7 @@ __device__ __forceinline__ void rec_tile64_i8(const DevState &st, Rec64Lds &L, i
       __syncthreads();
     }
   }
-  rec_quadrant_epilogue(st, T, v0, row, R, src, y, ax, F, hn, ne, wcol, wval);
+  rec_quadrant_epilogue(st, T, v0, row, R, src, ax, ew4, ev, ne, wcol, wval);
 }
 
 // Persistent exact bf16 recurrence over the active tiles (RecWalk): 64 x 64
