@@ -45,6 +45,19 @@ def test_cfg4_full_size_sampled(gpu, sched, eps):
     sampled_parity(wl, g, length_sample(wl, 48), f"cfg4 full {sched} eps={eps}, 48 sampled", sched)
 
 
+@pytest.mark.parametrize("sched", ["var_stream", "fixed"])
+def test_cfg5_full_size_sampled(gpu, sched):
+    # Config 5 at full size: 8192 inputs, n = 256, k = 5, |V| = 64000,
+    # d = 1024, KV rows of 6 layers appended every step; 24 inputs over the
+    # length distribution (the 8 longest included) decoded by the oracle.
+    from synthgen import get_config
+    wl = make_workload(get_config(5))
+    g, st, dec = gpu_decode(wl, sched)
+    dec.close()
+    assert st["finished"] == len(wl.Lx) and st["hyps"] == sum(len(y) for y in g)
+    sampled_parity(wl, g, length_sample(wl, 24), f"cfg5 full {sched}, 24 sampled", sched)
+
+
 def _kv_reference(wl, dec_o, i, tokens):
     """KV rows of a candidate of input i with emitted `tokens`: row r is
     bf16(h_r . W_kv) with h_r the state computed at step r (teacher forced)."""

@@ -113,7 +113,7 @@ def test_deterministic(gpu):
         assert [(h.tokens, h.score) for h in ya] == [(h.tokens, h.score) for h in yb]
 
 
-@pytest.mark.parametrize("sched", ["var_stream", "var_batch"])
+@pytest.mark.parametrize("sched", ["var_stream", "var_batch", "fixed", "var_fifo"])
 def test_cfg3_full_size_sampled(gpu, sched):
     # The full MT-shaped fp32 workload (4096 inputs, n = 128, |V| = 32000)
     # in the configuration the benchmark runs; 64 inputs spread over the
