@@ -1,7 +1,9 @@
 // Recurrence of the synthetic decoder D (Sec. 2) on gfx950 MFMA:
 //   h = tanh(W_h h_prev + E[y])      [R,d] x [d,d]^T, fused epilogue
 // W_h (out-feature rows) is the MFMA A operand and the previous states the B
-// operand, both K-contiguous. bf16 workloads accumulate in fp64 (see k_rec_bf16).
+// operand, both K-contiguous. bf16 workloads form the pre-activation
+// exactly from int8 digit products (k_rec_i8, below), or, where that does
+// not apply, accumulate it with the fp64 MFMA (rec_tile_bf16).
 #include <algorithm>
 #include <type_traits>
 
@@ -288,7 +290,7 @@ __device__ __forceinline__ AuxRegs load_aux(const RowAux *ax) {
   return r;
 }
 
-// Digit planes and list of the state feeding row r.
+// Digit planes (rec_dig_off layout) and list of the state feeding row r.
 __device__ __forceinline__ const int8_t *row_digits(const DevState &st, int r) {
   const int src = st.r_hsrc[r];
   return (src >= 0 ? st.s_hd : st.q_hd) + (size_t)(src >= 0 ? src : -1 - src) * rec_dig_row_bytes(st.d);
